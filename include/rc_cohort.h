@@ -1,0 +1,193 @@
+/*
+ * rc_cohort.h -- C ABI of the batched ready-cohort control transition,
+ * implemented with hand-written HIP kernels for AMD Instinct MI355X (gfx950).
+ *
+ * What the library computes.  A session holds W uint32 state words and one
+ * pending outcome.  Sessions are grouped into cohorts (contiguous session
+ * ranges of at most 256).  One chained step of a cohort applies the paper's
+ * unit of control work to every member (Abstract; Section 2 "Unit of
+ * execution": read typed state and an available outcome, route it, update the
+ * state, emit the next effect) with the decision made on the GPU (Section 7
+ * "Matched mechanisms": a GPU predicate selects one of two route bodies), and
+ * orders the emitted effects by a per-cohort compaction (Section 11
+ * "Mechanism and sampling scope" names per-event compaction and effect
+ * ordering as what a route service still needs).  Per session s, at step
+ * number `step`, with o its pending outcome and all arithmetic modulo 2^32:
+ *
+ *   route   r = o mod R                          (RC_ROUTE_MOD)
+ *           r = #{k < R-1 : route_cdf[k] <= o}   (RC_ROUTE_CDF)
+ *   decide  d = (fmix32(S[0] ^ o ^ step) & 0xFFFF) < decide_thr, on the
+ *           state before the update; fmix32 is MurmurHash3's finalizer
+ *   update  d = 1: S[w] ^= table[r][w mod 16] * (w + 1)       for all w < W
+ *           d = 0: S[w]  = rotl(S[w], (r + 1) mod 32) + o     for all w < W
+ *   emit    effect (sid = s, tool = table[r][d] mod 8, payload = S[0..3]
+ *           after the update) at the session's slot of the stable partition
+ *           of its cohort: taken sessions first, each group in ascending sid
+ *   count   n_taken[t][c] = taken sessions of cohort c at chained step t
+ *   chain   the session's next outcome is fmix32(S[0])
+ *
+ * Chaining T steps with the decision kept on the device (RC_MODE_RESIDENT)
+ * is the device-resident mechanism of Section 7; RC_MODE_HOST_ROUNDTRIP
+ * copies a 4-byte decision word to the host after every step and lets the
+ * host select and launch the route-body kernels (the host round trip of
+ * Section 7).  Both produce bit-identical outputs.
+ *
+ * Conventions.  All functions are extern "C", return an rc_status and never
+ * throw or abort.  RC_E_INVALID is detected on the host before anything is
+ * enqueued, so no caller buffer is touched.  After RC_E_DEVICE the contents
+ * of the output buffers are unspecified, but the handle stays valid and can
+ * be destroyed.  A handle must not be used by two threads at once.
+ */
+#ifndef RC_COHORT_H
+#define RC_COHORT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct rc_cohort rc_cohort; /* opaque; owned by the library */
+
+enum rc_status {
+    RC_OK = 0,
+    RC_E_INVALID = 1, /* bad argument; detected before any GPU work        */
+    RC_E_NOMEM = 2,   /* host or device allocation failed                 */
+    RC_E_DEVICE = 3   /* no usable gfx950 device, or a HIP call failed      */
+};
+
+enum rc_route_mode {
+    RC_ROUTE_MOD = 0, /* r = o mod R                                       */
+    RC_ROUTE_CDF = 1  /* r = number of route_cdf thresholds <= o            */
+};
+
+enum rc_chain_mode {
+    RC_MODE_RESIDENT = 0,      /* one launch; decisions never leave the GPU */
+    RC_MODE_HOST_ROUNDTRIP = 1 /* per step: decide kernel, 4-byte copy to
+                                  pinned host memory, stream sync, host
+                                  launches the selected body kernels        */
+};
+
+#define RC_MIN_WORDS 4u      /* the payload needs words 0..3 */
+#define RC_MAX_WORDS 64u
+#define RC_MAX_ROUTES 1024u
+#define RC_MAX_COHORT 256u
+#define RC_MAX_SESSIONS (1u << 30)
+
+/*
+ * Problem description (the paper's problem statement: sessions with typed
+ * state, route keys derived from outcomes, cohorts of size K; Sections 2-3).
+ * Every pointer is HOST memory read only during rc_cohort_create; the
+ * library copies what it needs and the caller keeps ownership.
+ */
+typedef struct rc_cohort_desc {
+    uint32_t n_sessions;            /* N, 1 <= N <= RC_MAX_SESSIONS          */
+    uint32_t n_words;               /* W, RC_MIN_WORDS <= W <= RC_MAX_WORDS   */
+    uint32_t n_routes;              /* R, 1 <= R <= RC_MAX_ROUTES             */
+    uint32_t n_cohorts;             /* C >= 1                                 */
+    const uint32_t *cohort_offsets; /* [C+1]: 0 = b_0 < b_1 < ... < b_C = N;
+                                       cohort c is sessions [b_c, b_{c+1}),
+                                       of size 1..RC_MAX_COHORT              */
+    const uint32_t *table;          /* [R][16] row-major transition table    */
+    uint32_t route_mode;            /* enum rc_route_mode                     */
+    const uint32_t *route_cdf;      /* [R-1] nondecreasing thresholds in CDF
+                                       mode (may be NULL when R == 1);
+                                       ignored in MOD mode                   */
+    uint32_t decide_thr;            /* 0..65536; 0 = never taken,
+                                       65536 = always taken                  */
+} rc_cohort_desc;
+
+/*
+ * Caller-owned DEVICE buffers on the handle's device, structure of arrays
+ * with leading dimension ld >= N.  For a call that runs T steps:
+ *   state        [W][ld]     in/out  word w of session s at state[w*ld + s]
+ *   outcome      [ld]        in/out  pending outcome; on return the outcome
+ *                                    for the step after the last one
+ *   eff_sid      [T][ld]     out     effect slice t, slot j at [t*ld + j]
+ *   eff_tool     [T][ld]     out
+ *   eff_payload  [T][4][ld]  out     payload word q at [(t*4 + q)*ld + j]
+ *   n_taken      [T][C]      out     at [t*C + c]
+ * Effect slice t of a call is written at the slice offsets above relative
+ * to the pointers passed; a caller chaining several calls into one log
+ * passes pointers advanced by the slices already written.  The six buffers
+ * must not overlap (checked).  Only the sessions, effect slots and n_taken
+ * entries of the cohorts in [cohort_begin, cohort_end) are written; every
+ * other element, including the padding columns [N, ld), stays unchanged.
+ */
+typedef struct rc_buffers {
+    uint32_t *state;
+    uint32_t *outcome;
+    uint32_t *eff_sid;
+    uint32_t *eff_tool;
+    uint32_t *eff_payload;
+    uint32_t *n_taken;
+    uint32_t ld;
+} rc_buffers;
+
+/*
+ * Validate `desc`, then bind to HIP device `hip_device` (an ordinal), copy
+ * the cohort offsets, table and thresholds to device memory the library
+ * owns, and build the launch plan (which cohorts share a workgroup).
+ * Writes the new handle to *out (left untouched on error).
+ * Errors: RC_E_INVALID for a bad descriptor or out == NULL (checked before
+ * any device call); RC_E_DEVICE when the device does not exist or is not a
+ * gfx950; RC_E_NOMEM when an allocation fails.
+ */
+int rc_cohort_create(const rc_cohort_desc *desc, int hip_device, rc_cohort **out);
+
+/*
+ * One step (T = 1) of the cohorts [cohort_begin, cohort_end) with step
+ * number `step`, in resident mode: exactly rc_cohort_run_chain(h, b, step,
+ * 1, RC_MODE_RESIDENT, cohort_begin, cohort_end, hip_stream).
+ */
+int rc_cohort_step(rc_cohort *h, const rc_buffers *b, uint32_t step,
+                   uint32_t cohort_begin, uint32_t cohort_end, void *hip_stream);
+
+/*
+ * n_steps chained steps of the cohorts [cohort_begin, cohort_end); step t
+ * (0-based) uses the step number step0 + t (mod 2^32).  `hip_stream` is a
+ * hipStream_t of the handle's device (NULL = the null stream).
+ * RC_MODE_RESIDENT enqueues one kernel launch and returns without waiting.
+ * RC_MODE_HOST_ROUNDTRIP synchronizes the stream once per step (that
+ * observation is the mechanism being measured) and returns after enqueuing
+ * the last body kernel.  n_steps == 0 or an empty cohort range is a no-op.
+ * Chains compose: (T1 steps from step0) then (T2 steps from step0 + T1)
+ * equals T1 + T2 steps from step0.
+ * Errors: RC_E_INVALID for a NULL handle/buffer, ld < N, a bad range or
+ * mode, overlapping buffers, or a buffer that is not device memory of the
+ * handle's device large enough for its extent; RC_E_DEVICE when a launch or
+ * copy fails.
+ */
+int rc_cohort_run_chain(rc_cohort *h, const rc_buffers *b, uint32_t step0,
+                        uint32_t n_steps, int mode, uint32_t cohort_begin,
+                        uint32_t cohort_end, void *hip_stream);
+
+/* Release the handle's device and host resources.  Waits for nothing: the
+ * caller synchronizes its streams first.  rc_cohort_destroy(NULL) is RC_OK. */
+int rc_cohort_destroy(rc_cohort *h);
+
+/* Static, NUL-terminated name of a status code ("RC_OK", ...). */
+const char *rc_status_string(int status);
+
+/*
+ * Kernel launches and device-to-host copies enqueued by the last successful
+ * rc_cohort_run_chain / rc_cohort_step on this handle (resident: 1 and 0;
+ * host round trip: at least T + 1 launches and exactly T copies).  Either
+ * output pointer may be NULL.  RC_E_INVALID when h is NULL.
+ */
+int rc_cohort_last_counts(const rc_cohort *h, uint32_t *launches, uint32_t *d2h_copies);
+
+/*
+ * Launch-plan summary: workgroups in the plan, lanes per workgroup, and
+ * lanes left idle by packing (cohorts never straddle a workgroup, and a
+ * cohort of at most 64 sessions never straddles a wavefront).  Any output
+ * pointer may be NULL.  RC_E_INVALID when h is NULL.
+ */
+int rc_cohort_plan_info(const rc_cohort *h, uint32_t *n_workgroups,
+                        uint32_t *lanes_per_workgroup, uint32_t *idle_lanes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RC_COHORT_H */

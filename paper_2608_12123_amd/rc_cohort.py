@@ -1,0 +1,279 @@
+"""Thin Python binding of ``librc_cohort.so`` (the C ABI in include/rc_cohort.h).
+
+Argument marshalling only: every step of the transition runs in the HIP
+kernels.  There is no CPU fallback -- if the library is missing or no gfx950
+device is usable, the calls raise.
+
+The function names are those of the C ABI (``rc_cohort_create``,
+``rc_cohort_step``, ``rc_cohort_run_chain``, ``rc_cohort_destroy``, ...).
+Device buffers are torch int32 tensors (PyTorch supplies device memory and
+streams); uint32 values are carried bit-for-bit in int32 storage.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "librc_cohort.so")
+
+RC_OK, RC_E_INVALID, RC_E_NOMEM, RC_E_DEVICE = 0, 1, 2, 3
+RC_ROUTE_MOD, RC_ROUTE_CDF = 0, 1
+RC_MODE_RESIDENT, RC_MODE_HOST_ROUNDTRIP = 0, 1
+
+EXPORTED = [
+    "rc_cohort_create", "rc_cohort_step", "rc_cohort_run_chain", "rc_cohort_destroy",
+    "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info",
+]
+
+_P32 = ctypes.POINTER(ctypes.c_uint32)
+
+
+class RcCohortDesc(ctypes.Structure):
+    _fields_ = [
+        ("n_sessions", ctypes.c_uint32),
+        ("n_words", ctypes.c_uint32),
+        ("n_routes", ctypes.c_uint32),
+        ("n_cohorts", ctypes.c_uint32),
+        ("cohort_offsets", _P32),
+        ("table", _P32),
+        ("route_mode", ctypes.c_uint32),
+        ("route_cdf", _P32),
+        ("decide_thr", ctypes.c_uint32),
+    ]
+
+
+class RcBuffers(ctypes.Structure):
+    _fields_ = [
+        ("state", ctypes.c_void_p),
+        ("outcome", ctypes.c_void_p),
+        ("eff_sid", ctypes.c_void_p),
+        ("eff_tool", ctypes.c_void_p),
+        ("eff_payload", ctypes.c_void_p),
+        ("n_taken", ctypes.c_void_p),
+        ("ld", ctypes.c_uint32),
+    ]
+
+
+class RcError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s failed: %s" % (what, rc_status_string(status)))
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the built HIP library.  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            "librc_cohort.so is not built (run paper_2608_12123_amd/build.py or "
+            "__graft_entry__.build()); there is no CPU fallback")
+    lib = ctypes.CDLL(path)
+    lib.rc_cohort_create.argtypes = [ctypes.POINTER(RcCohortDesc), ctypes.c_int,
+                                     ctypes.POINTER(ctypes.c_void_p)]
+    lib.rc_cohort_create.restype = ctypes.c_int
+    lib.rc_cohort_step.argtypes = [ctypes.c_void_p, ctypes.POINTER(RcBuffers), ctypes.c_uint32,
+                                   ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p]
+    lib.rc_cohort_step.restype = ctypes.c_int
+    lib.rc_cohort_run_chain.argtypes = [ctypes.c_void_p, ctypes.POINTER(RcBuffers), ctypes.c_uint32,
+                                        ctypes.c_uint32, ctypes.c_int, ctypes.c_uint32,
+                                        ctypes.c_uint32, ctypes.c_void_p]
+    lib.rc_cohort_run_chain.restype = ctypes.c_int
+    lib.rc_cohort_destroy.argtypes = [ctypes.c_void_p]
+    lib.rc_cohort_destroy.restype = ctypes.c_int
+    lib.rc_status_string.argtypes = [ctypes.c_int]
+    lib.rc_status_string.restype = ctypes.c_char_p
+    lib.rc_cohort_last_counts.argtypes = [ctypes.c_void_p, _P32, _P32]
+    lib.rc_cohort_last_counts.restype = ctypes.c_int
+    lib.rc_cohort_plan_info.argtypes = [ctypes.c_void_p, _P32, _P32, _P32]
+    lib.rc_cohort_plan_info.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _u32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.uint32))
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(_P32)
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def rc_status_string(status: int) -> str:
+    return load_library().rc_status_string(status).decode()
+
+
+def _check(status: int, what: str):
+    if status != RC_OK:
+        raise RcError(status, what)
+
+
+def rc_cohort_create(*, n_sessions: int, n_words: int, n_routes: int, cohort_offsets,
+                     table, route_mode: int, route_cdf, decide_thr: int, device: int = 0,
+                     check: bool = True):
+    """Create a handle; returns (status, handle) when ``check`` is False."""
+    lib = load_library()
+    off = _u32(cohort_offsets)
+    tab = _u32(table).reshape(-1)
+    cdf = None if route_cdf is None else _u32(route_cdf)
+    desc = RcCohortDesc(n_sessions, n_words, n_routes, off.size - 1, _ptr(off), _ptr(tab),
+                        route_mode, _ptr(cdf), decide_thr)
+    h = ctypes.c_void_p()
+    st = lib.rc_cohort_create(ctypes.byref(desc), device, ctypes.byref(h))
+    if not check:
+        return st, h
+    _check(st, "rc_cohort_create")
+    return h
+
+
+def rc_cohort_step(h, buffers: RcBuffers, step: int, cohort_begin: int, cohort_end: int,
+                   stream=None, check: bool = True) -> int:
+    st = load_library().rc_cohort_step(h, ctypes.byref(buffers), step & 0xFFFFFFFF,
+                                       cohort_begin, cohort_end, _stream_handle(stream))
+    if check:
+        _check(st, "rc_cohort_step")
+    return st
+
+
+def rc_cohort_run_chain(h, buffers: RcBuffers, step0: int, n_steps: int, mode: int,
+                        cohort_begin: int, cohort_end: int, stream=None,
+                        check: bool = True) -> int:
+    st = load_library().rc_cohort_run_chain(h, ctypes.byref(buffers), step0 & 0xFFFFFFFF,
+                                            n_steps, mode, cohort_begin, cohort_end,
+                                            _stream_handle(stream))
+    if check:
+        _check(st, "rc_cohort_run_chain")
+    return st
+
+
+def rc_cohort_destroy(h) -> int:
+    return load_library().rc_cohort_destroy(h)
+
+
+def rc_cohort_last_counts(h):
+    a, b = ctypes.c_uint32(), ctypes.c_uint32()
+    _check(load_library().rc_cohort_last_counts(h, ctypes.byref(a), ctypes.byref(b)),
+           "rc_cohort_last_counts")
+    return a.value, b.value
+
+
+def rc_cohort_plan_info(h):
+    a, b, c = ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32()
+    _check(load_library().rc_cohort_plan_info(h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)),
+           "rc_cohort_plan_info")
+    return a.value, b.value, c.value
+
+
+# ---------------------------------------------------------------------------
+# Device buffers (torch) for one handle
+# ---------------------------------------------------------------------------
+def _to_device_u32(arr: np.ndarray, device):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.uint32).view(np.int32)).to(device)
+
+
+def _to_host_u32(t) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint32)
+
+
+def buffers_of(tensors: Dict[str, "object"], ld: int) -> RcBuffers:
+    """An ``RcBuffers`` pointing at torch tensors (keys as in the C struct)."""
+    return RcBuffers(tensors["state"].data_ptr(), tensors["outcome"].data_ptr(),
+                     tensors["eff_sid"].data_ptr(), tensors["eff_tool"].data_ptr(),
+                     tensors["eff_payload"].data_ptr(), tensors["n_taken"].data_ptr(), ld)
+
+
+class Cohort:
+    """A handle plus torch device buffers sized for chains of up to
+    ``max_steps`` steps.  State and outcome are uploaded from host arrays
+    (uint32, ``[W][ld]`` and ``[ld]``)."""
+
+    def __init__(self, *, n_words, n_routes, cohort_offsets, table, route_mode, route_cdf,
+                 decide_thr, max_steps, ld=None, device=0, fill=0xFFFFFFFF):
+        import torch
+        self.device = torch.device("cuda", device)
+        off = _u32(cohort_offsets)
+        self.n_sessions = int(off[-1])
+        self.n_cohorts = off.size - 1
+        self.n_words = n_words
+        self.ld = self.n_sessions if ld is None else ld
+        self.max_steps = max_steps
+        self.handle = rc_cohort_create(n_sessions=self.n_sessions, n_words=n_words,
+                                       n_routes=n_routes, cohort_offsets=off, table=table,
+                                       route_mode=route_mode, route_cdf=route_cdf,
+                                       decide_thr=decide_thr, device=device)
+        fill32 = np.uint32(fill).view(np.int32).item()
+        T, ld, C = max_steps, self.ld, self.n_cohorts
+        mk = lambda *shape: torch.full(shape, fill32, dtype=torch.int32, device=self.device)
+        self.t = {"state": mk(n_words, ld), "outcome": mk(ld), "eff_sid": mk(T, ld),
+                  "eff_tool": mk(T, ld), "eff_payload": mk(T, 4, ld), "n_taken": mk(T, C)}
+        self.buffers = buffers_of(self.t, ld)
+
+    @classmethod
+    def from_inputs(cls, inp, max_steps=None, device=0):
+        c = cls(n_words=inp.n_words, n_routes=inp.n_routes, cohort_offsets=inp.cohort_offsets,
+                table=inp.table, route_mode=inp.route_mode, route_cdf=inp.route_cdf,
+                decide_thr=inp.decide_thr, max_steps=max_steps or inp.n_steps, ld=inp.ld,
+                device=device)
+        c.upload(inp.state, inp.outcome)
+        return c
+
+    def upload(self, state: np.ndarray, outcome: np.ndarray):
+        assert state.shape == (self.n_words, self.ld) and outcome.shape == (self.ld,)
+        self.t["state"].copy_(_to_device_u32(state, self.device))
+        self.t["outcome"].copy_(_to_device_u32(outcome, self.device))
+
+    def run_chain(self, step0, n_steps, mode=RC_MODE_RESIDENT, cohort_begin=0, cohort_end=None,
+                  stream=None):
+        assert n_steps <= self.max_steps
+        ce = self.n_cohorts if cohort_end is None else cohort_end
+        return rc_cohort_run_chain(self.handle, self.buffers, step0, n_steps, mode, cohort_begin,
+                                   ce, stream)
+
+    def step(self, step, cohort_begin=0, cohort_end=None, stream=None):
+        ce = self.n_cohorts if cohort_end is None else cohort_end
+        return rc_cohort_step(self.handle, self.buffers, step, cohort_begin, ce, stream)
+
+    def download(self, n_steps=None) -> Dict[str, np.ndarray]:
+        import torch
+        torch.cuda.synchronize(self.device)
+        T = self.max_steps if n_steps is None else n_steps
+        return {"state": _to_host_u32(self.t["state"]), "outcome": _to_host_u32(self.t["outcome"]),
+                "eff_sid": _to_host_u32(self.t["eff_sid"][:T]),
+                "eff_tool": _to_host_u32(self.t["eff_tool"][:T]),
+                "eff_payload": _to_host_u32(self.t["eff_payload"][:T]),
+                "n_taken": _to_host_u32(self.t["n_taken"][:T])}
+
+    def last_counts(self):
+        return rc_cohort_last_counts(self.handle)
+
+    def plan_info(self):
+        return rc_cohort_plan_info(self.handle)
+
+    def close(self):
+        if self.handle is not None:
+            rc_cohort_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
