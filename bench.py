@@ -1,0 +1,373 @@
+"""Benchmark of the batched ready-cohort transition on one MI355X.
+
+Default run (no flags): the 100,000-session workload (391 cohorts of K=256,
+W=32, R=256, p=0.5, T=16 chained steps) -- the throughput / HBM-bandwidth
+workload.  One bench step is one device-resident chain over all sessions
+(every step of the hot path: route, decide, compact, update, emit, chain).
+It prints ONE JSON line with the contract fields plus:
+
+* ``host_roundtrip``: the same workload through the host-round-trip
+  mechanism (4-byte readback + host branch + relaunch every chained step);
+* ``mechanisms``: resident vs host round trip on all five workloads
+  (microseconds per invocation and per chained step, launches and
+  device-to-host copies per invocation);
+* ``roofline``: algorithmic bytes per launch of the resident chain kernel
+  over its average duration, timed with HIP events on the launch stream;
+* ``cpu_baseline``: the single-threaded CPU oracle on the same workload.
+
+Inputs are synthetic and seeded (see paper_2608_12123_amd/workload.py).  The
+timed region rotates through enough buffer sets that the working set is
+larger than the 256 MB Infinity Cache.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("transitions/sec and µs per chained cohort step (resident vs host round trip); "
+          "HBM GB/s")
+HBM_PEAK_GBS = 8000.0
+INFINITY_CACHE_BYTES = 256 << 20
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "rc_chain_kernel_s100k_traffic.txt")
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_12123_amd", "csrc", "rc_cohort.hip")
+
+
+def algorithmic_bytes(n_sessions, n_words, n_steps, n_cohorts):
+    """Bytes the resident chain must move per launch: state and outcome read
+    and written once per chain, one 24-byte effect per transition, and the
+    per-cohort taken counts.  The route table (read from L2 into LDS) is not
+    counted."""
+    state = 2 * 4 * n_words * n_sessions
+    outcome = 2 * 4 * n_sessions
+    effects = 24 * n_sessions * n_steps
+    counts = 4 * n_steps * n_cohorts
+    return state + outcome + effects + counts
+
+
+def kernel_src_hash():
+    import hashlib
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def stored_traffic(steps_hint):
+    """HBM traffic per launch from the committed rocprofv3 counter summary,
+    valid only while the kernel source is unchanged."""
+    if not os.path.exists(PROFILE_TRAFFIC):
+        return None
+    vals = {}
+    with open(PROFILE_TRAFFIC) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_src_sha256_16") != kernel_src_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+class Sets:
+    """Rotating device buffer sets for one handle."""
+
+    def __init__(self, rc, inp, n_steps, n_sets):
+        import torch
+        self.inp = inp
+        self.sets = []
+        for _ in range(n_sets):
+            t = {
+                "state": torch.from_numpy(inp.state.view(np.int32)).cuda(),
+                "outcome": torch.from_numpy(inp.outcome.view(np.int32)).cuda(),
+                "eff_sid": torch.empty((n_steps, inp.ld), dtype=torch.int32, device="cuda"),
+                "eff_tool": torch.empty((n_steps, inp.ld), dtype=torch.int32, device="cuda"),
+                "eff_payload": torch.empty((n_steps, 4, inp.ld), dtype=torch.int32, device="cuda"),
+                "n_taken": torch.empty((n_steps, inp.n_cohorts), dtype=torch.int32, device="cuda"),
+            }
+            self.sets.append((t, rc.buffers_of(t, inp.ld)))
+
+    def bytes_per_set(self):
+        return sum(v.numel() * 4 for v in self.sets[0][0].values())
+
+    def __getitem__(self, i):
+        return self.sets[i % len(self.sets)][1]
+
+    def tensors(self, i):
+        return self.sets[i % len(self.sets)][0]
+
+
+def n_sets_for(bytes_per_set, min_total=2 * INFINITY_CACHE_BYTES, cap=16):
+    return int(max(2, min(cap, -(-min_total // max(1, bytes_per_set)))))
+
+
+def time_resident(rc, h, sets, inp, T, steps, warmup, stream, ranges=None, events=True):
+    """Pipelined resident chains; returns wall seconds and per-launch kernel ms."""
+    import torch
+    C = inp.n_cohorts
+    rng = ranges or [(0, C)]
+    for i in range(warmup):
+        cb, ce = rng[i % len(rng)]
+        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_RESIDENT, cb, ce, stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)] if events else None
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        cb, ce = rng[i % len(rng)]
+        if events:
+            ev[i][0].record()
+        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_RESIDENT, cb, ce, stream)
+        if events:
+            ev[i][1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kms = [a.elapsed_time(b) for a, b in ev] if events else []
+    return wall, kms
+
+
+def time_resident_synced(rc, h, sets, inp, T, steps, stream, ranges):
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        cb, ce = ranges[i % len(ranges)]
+        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_RESIDENT, cb, ce, stream)
+        torch.cuda.current_stream().synchronize()
+    return time.perf_counter() - t0
+
+
+def time_hrt(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
+    import torch
+    C = inp.n_cohorts
+    rng = ranges or [(0, C)]
+    for i in range(warmup):
+        cb, ce = rng[i % len(rng)]
+        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, cb, ce, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        cb, ce = rng[i % len(rng)]
+        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, cb, ce, stream)
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
+def mechanism_row(rc, wk, key, budget_s=1.0):
+    """Resident (pipelined and synchronized) vs host round trip on one
+    workload; invocations as the workload defines them."""
+    import torch
+    wl = wk.WORKLOADS[key]
+    inp = wk.make_inputs(wl)
+    T = wl.n_steps
+    h = rc.rc_cohort_create(n_sessions=inp.n_sessions, n_words=inp.n_words, n_routes=inp.n_routes,
+                            cohort_offsets=inp.cohort_offsets, table=inp.table,
+                            route_mode=inp.route_mode, route_cdf=inp.route_cdf,
+                            decide_thr=inp.decide_thr)
+    try:
+        if wl.per_cohort_invocation:
+            ranges = [(c, c + 1) for c in range(inp.n_cohorts)]
+            per_inv = wl.cohort_size * T
+        else:
+            ranges = [(0, inp.n_cohorts)]
+            per_inv = inp.n_sessions * T
+        sets = Sets(rc, inp, T, 1 if wl.per_cohort_invocation else 2)
+        stream = torch.cuda.current_stream().cuda_stream
+        # calibrate the invocation count on the faster (resident) mechanism
+        w, _ = time_resident(rc, h, sets, inp, T, 20, 5, stream, ranges, events=False)
+        n = int(max(20, min(20000, budget_s / 3 / max(w / 20, 1e-7))))
+        wall_r, _ = time_resident(rc, h, sets, inp, T, n, 5, stream, ranges, events=False)
+        rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_RESIDENT, *ranges[0], stream)
+        res_counts = rc.rc_cohort_last_counts(h)
+        n_sync = max(10, n // 4)
+        wall_s = time_resident_synced(rc, h, sets, inp, T, n_sync, stream, ranges)
+        w1 = time_hrt(rc, h, sets, inp, T, 3, 1, stream, ranges)
+        n_h = int(max(5, min(n, budget_s / 2 / max(w1 / 3, 1e-7))))
+        wall_h = time_hrt(rc, h, sets, inp, T, n_h, 0, stream, ranges)
+        rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, *ranges[0], stream)
+        hrt_counts = rc.rc_cohort_last_counts(h)
+        torch.cuda.synchronize()
+    finally:
+        rc.rc_cohort_destroy(h)
+    us_r, us_s, us_h = wall_r / n * 1e6, wall_s / n_sync * 1e6, wall_h / n_h * 1e6
+    return {
+        "workload": wl.title, "T": T, "transitions_per_invocation": per_inv,
+        "resident_us_per_invocation": round(us_r, 3),
+        "resident_us_per_chained_step": round(us_r / T, 4),
+        "resident_synced_us_per_invocation": round(us_s, 3),
+        "host_rt_us_per_invocation": round(us_h, 3),
+        "host_rt_us_per_chained_step": round(us_h / T, 4),
+        "host_over_resident": round(us_h / us_r, 3),
+        "host_over_resident_synced": round(us_h / us_s, 3),
+        "resident_transitions_per_s": round(per_inv / (us_r * 1e-6), 1),
+        "host_rt_transitions_per_s": round(per_inv / (us_h * 1e-6), 1),
+        "launches_per_invocation": {"resident": res_counts[0], "host_rt": hrt_counts[0]},
+        "d2h_copies_per_invocation": {"resident": res_counts[1], "host_rt": hrt_counts[1]},
+        "invocations_timed": {"resident": n, "resident_synced": n_sync, "host_rt": n_h},
+    }
+
+
+def cpu_baseline(inp, T, min_seconds):
+    """The oracle (plain single-threaded C) on the same workload, repeated
+    until at least ``min_seconds`` of CPU work; also returns its outputs of
+    the first repetition for the parity check of this run."""
+    import oracle
+    orc = oracle.load()
+    reps, first = 0, None
+    t0 = time.perf_counter()
+    while True:
+        out = orc.run_inputs(inp, n_steps=T)
+        if first is None:
+            first = out
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    trans = reps * inp.n_sessions * T
+    return {"value": round(trans / el, 1), "unit": "transitions/s", "cores": 1, "kind": "oracle",
+            "sample": "full workload (%d sessions x %d chained steps), %d repetition(s), %.1f s, "
+                      "single thread, gcc -O2; host %s, %d logical CPUs"
+                      % (inp.n_sessions, T, reps, el, platform.processor() or platform.machine(),
+                         os.cpu_count() or 0)}, first
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default="s100k",
+                    help="workload of the headline line (tiny, k64, k256, s100k, s1m)")
+    ap.add_argument("--hrt-steps", type=int, default=200)
+    ap.add_argument("--no-mechanisms", action="store_true", help="skip the five-workload table")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="only the resident timed loop (for rocprofv3 counter runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only a plain device-to-device copy of known size (HBM counter scale)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(cohorts are independent; see the sharding design). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if args.copy_calibration:
+        n = 128 << 20  # 512 MiB of int32
+        src = torch.ones(n, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read_per_dispatch": n * 4,
+                          "bytes_written_per_dispatch": n * 4, "dispatches": 5}), flush=True)
+        return
+
+    from paper_2608_12123_amd import rc_cohort as rc
+    from paper_2608_12123_amd import workload as wk
+
+    assert torch.cuda.is_available(), "bench.py needs an MI355X"
+    rc.load_library()
+    wl = wk.WORKLOADS[args.workload]
+    inp = wk.make_inputs(wl)
+    T = wl.n_steps
+    N, C, W = inp.n_sessions, inp.n_cohorts, inp.n_words
+    h = rc.rc_cohort_create(n_sessions=N, n_words=W, n_routes=inp.n_routes,
+                            cohort_offsets=inp.cohort_offsets, table=inp.table,
+                            route_mode=inp.route_mode, route_cdf=inp.route_cdf,
+                            decide_thr=inp.decide_thr)
+    stream = torch.cuda.current_stream().cuda_stream
+    probe = Sets(rc, inp, T, 1)
+    n_sets = n_sets_for(probe.bytes_per_set())
+    del probe
+    sets = Sets(rc, inp, T, n_sets)
+    plan = rc.rc_cohort_plan_info(h)
+
+    # parity of this run's kernel on fresh inputs against the oracle
+    verified = None
+    cpu = None
+    if not args.profile_only and not args.no_cpu_baseline:
+        cpu, want = cpu_baseline(inp, T, args.cpu_seconds)
+        rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_RESIDENT, 0, C, stream)
+        torch.cuda.synchronize()
+        t = sets.tensors(0)
+        verified = all(np.array_equal(t[k].cpu().numpy().view(np.uint32), want[k]) for k in want)
+        sets = Sets(rc, inp, T, n_sets)  # fresh inputs again
+
+    wall, kms = time_resident(rc, h, sets, inp, T, args.steps, args.warmup, stream)
+    trans_per_step = N * T
+    value = trans_per_step * args.steps / wall
+    ms_per_step = wall / args.steps * 1e3
+    k_avg_ms = statistics.fmean(kms)
+    k_med_ms = statistics.median(kms)
+    abytes = algorithmic_bytes(N, W, T, C)
+    achieved = abytes / (k_avg_ms * 1e-3) / 1e9
+    traffic = stored_traffic(args.steps)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "transitions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic (seeded SplitMix64 inputs; no trace data)",
+        "config": {
+            "workload": wl.title, "sessions": N, "cohorts": C, "W": W, "R": inp.n_routes,
+            "route_map": "mod" if inp.route_mode == wk.ROUTE_MOD else "zipf-cdf",
+            "decide_thr": inp.decide_thr, "T": T, "mode": "device-resident chain",
+            "parallelism": "single GPU", "buffer_sets_rotated": n_sets,
+            "plan": {"workgroups": plan[0], "lanes_per_workgroup": plan[1], "idle_lanes": plan[2]},
+        },
+        "us_per_chained_step": round(ms_per_step * 1e3 / T, 4),
+        "kernel_us": {"avg": round(k_avg_ms * 1e3, 3), "median": round(k_med_ms * 1e3, 3)},
+        "roofline": {
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "kernel": "rc_chain_kernel", "algorithmic_bytes_per_launch": abytes,
+        },
+        "verified_vs_oracle": verified,
+    }
+    if not args.profile_only:
+        hs = max(5, min(args.hrt_steps, args.steps))
+        wall_h = time_hrt(rc, h, sets, inp, T, hs, 3, stream)
+        rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, 0, C, stream)
+        cnt = rc.rc_cohort_last_counts(h)
+        us_h = wall_h / hs * 1e6
+        out["host_roundtrip"] = {
+            "value": round(trans_per_step / (us_h * 1e-6), 1), "unit": "transitions/s",
+            "us_per_invocation": round(us_h, 3), "us_per_chained_step": round(us_h / T, 4),
+            "host_over_resident": round(us_h / (ms_per_step * 1e3), 3),
+            "launches_per_invocation": cnt[0], "d2h_copies_per_invocation": cnt[1], "steps": hs,
+        }
+        if cpu is not None:
+            out["cpu_baseline"] = cpu
+        if not args.no_mechanisms:
+            out["mechanisms"] = {k: mechanism_row(rc, wk, k) for k in wk.WORKLOAD_ORDER}
+    rc.rc_cohort_destroy(h)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
