@@ -93,7 +93,7 @@ class Sets:
                 "outcome": torch.from_numpy(inp.outcome.view(np.int32)).cuda(),
                 "eff_sid": torch.empty((n_steps, inp.ld), dtype=torch.int32, device="cuda"),
                 "eff_tool": torch.empty((n_steps, inp.ld), dtype=torch.int32, device="cuda"),
-                "eff_payload": torch.empty((n_steps, 4, inp.ld), dtype=torch.int32, device="cuda"),
+                "eff_payload": torch.empty((n_steps, inp.ld, 4), dtype=torch.int32, device="cuda"),
                 "n_taken": torch.empty((n_steps, inp.n_cohorts), dtype=torch.int32, device="cuda"),
             }
             self.sets.append((t, rc.buffers_of(t, inp.ld)))

@@ -72,7 +72,7 @@ enum rc_chain_mode {
 #define RC_MAX_WORDS 64u
 #define RC_MAX_ROUTES 1024u
 #define RC_MAX_COHORT 256u
-#define RC_MAX_SESSIONS (1u << 30)
+#define RC_MAX_SESSIONS (1u << 28)
 
 /*
  * Problem description (the paper's problem statement: sessions with typed
@@ -105,7 +105,8 @@ typedef struct rc_cohort_desc {
  *                                    for the step after the last one
  *   eff_sid      [T][ld]     out     effect slice t, slot j at [t*ld + j]
  *   eff_tool     [T][ld]     out
- *   eff_payload  [T][4][ld]  out     payload word q at [(t*4 + q)*ld + j]
+ *   eff_payload  [T][ld][4]  out     payload word q at [(t*ld + j)*4 + q]
+ *                                    (16 contiguous bytes per effect)
  *   n_taken      [T][C]      out     at [t*C + c]
  * Effect slice t of a call is written at the slice offsets above relative
  * to the pointers passed; a caller chaining several calls into one log
@@ -185,6 +186,21 @@ int rc_cohort_last_counts(const rc_cohort *h, uint32_t *launches, uint32_t *d2h_
  */
 int rc_cohort_plan_info(const rc_cohort *h, uint32_t *n_workgroups,
                         uint32_t *lanes_per_workgroup, uint32_t *idle_lanes);
+
+/*
+ * Host-only inspection of the launch plan the library would build for
+ * `desc` with workgroups of `lanes_per_workgroup` lanes (256 or 512; the
+ * library picks one of these per handle).  No device is used.  Writes
+ * *n_lanes = bins * lanes_per_workgroup.  When both arrays are non-NULL
+ * (capacity >= *n_lanes entries each, host memory) it also writes, for every
+ * plan lane, the session it processes and that session's cohort, derived
+ * exactly as the kernels derive them (0xFFFFFFFF for idle lanes).  Every
+ * session appears in exactly one lane.  Errors: RC_E_INVALID for a bad
+ * descriptor, lane count, NULL n_lanes or too small a capacity.
+ */
+int rc_plan_lanes(const rc_cohort_desc *desc, uint32_t lanes_per_workgroup,
+                  uint32_t *lane_session, uint32_t *lane_cohort, uint32_t capacity,
+                  uint32_t *n_lanes);
 
 #ifdef __cplusplus
 }

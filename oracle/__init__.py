@@ -129,7 +129,7 @@ class Oracle:
 
         ``state`` is ``[W][ld]`` uint32 and ``outcome`` ``[ld]`` uint32; both
         are updated in place.  Effect arrays (``[T][ld]``, ``[T][ld]``,
-        ``[T][4][ld]``) and ``n_taken`` (``[T][C]``) are allocated filled with
+        ``[T][ld][4]``) and ``n_taken`` (``[T][C]``) are allocated filled with
         ``0xFFFFFFFF`` when not given.  Returns a dict of the output arrays.
         """
         offsets = _u32(cohort_offsets)
@@ -150,7 +150,7 @@ class Oracle:
         if eff_tool is None:
             eff_tool = np.full((T, ld), fill, dtype=np.uint32)
         if eff_payload is None:
-            eff_payload = np.full((T, 4, ld), fill, dtype=np.uint32)
+            eff_payload = np.full((T, ld, 4), fill, dtype=np.uint32)
         if n_taken is None:
             n_taken = np.full((T, n_cohorts), fill, dtype=np.uint32)
         rc = self.lib.rc_oracle_run_chain(

@@ -40,7 +40,7 @@
  *
  * Layout (structure of arrays, leading dimension ld >= N):
  *   state[w*ld + s], outcome[s], eff_sid[t*ld + slot], eff_tool[t*ld + slot],
- *   eff_payload[(t*4 + q)*ld + slot], n_taken[t*C + c].
+ *   eff_payload[(t*ld + slot)*4 + q], n_taken[t*C + c].
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -206,7 +206,7 @@ int rc_oracle_run_chain(uint32_t n_sessions, uint32_t n_words,
                 eff_sid[slice + slot] = s;
                 eff_tool[slice + slot] = table[r * 16u + d] % 8u;
                 for (q = 0u; q < 4u; ++q)
-                    eff_payload[((size_t)t * 4u + q) * ld + slot] =
+                    eff_payload[((size_t)t * ld + slot) * 4u + q] =
                         state[(size_t)q * ld + s];
                 outcome[s] = rc_oracle_fmix32(state[s]);
             }

@@ -2,6 +2,8 @@
 // MI355X (gfx950): hand-written HIP kernels and the C ABI of rc_cohort.h.
 //
 // Kernels
+//   rc_prep_kernel    once per handle: builds the route-table image that every
+//                     workgroup stages into LDS.
 //   rc_chain_kernel   device-resident chain (Section 7 "Device resident"):
 //                     one launch runs T chained steps; state lives in VGPRs,
 //                     decisions never leave the chip.
@@ -11,28 +13,49 @@
 //                     compacted list the host selected.
 //
 // Data layout (HBM, structure of arrays, leading dimension ld): state
-// [W][ld], outcome [ld], effects [T][ld] x {sid, tool} and [T][4][ld]
-// payload, n_taken [T][C].  A wavefront's 64 lanes touch 64 consecutive
-// sessions of one word row, so every state access is a fully coalesced
-// 256-byte row segment.
+// [W][ld], outcome [ld], effects [T][ld] for sid and tool, [T][ld][4] for the
+// payload, n_taken [T][C].  A wavefront's 64 lanes read 64 consecutive
+// sessions of one word row (a 256-byte segment); an effect's payload is one
+// 16-byte store.
 //
-// Launch plan (built on the host at create time).  Cohorts are packed in
-// order into workgroups ("bins") of 256 or 512 lanes.  A cohort of at most
-// 64 sessions never straddles a wavefront; a larger cohort starts on a
-// wavefront boundary and spans whole wavefronts; no cohort straddles a
-// workgroup.  Per wavefront the plan stores a 32-byte descriptor read with
-// scalar loads.  The compaction (stable partition, taken first) is a
-// wavefront ballot + mbcnt rank; a cohort spanning several wavefronts adds an
-// LDS exchange of per-wavefront popcounts behind one workgroup barrier per
-// step (double-buffered, so one barrier suffices).
+// Launch plan (built on the host at create time).  Cohorts of at most 64
+// sessions are packed, in order, into "sub-wavefront" bins that never need a
+// workgroup barrier; larger cohorts go, in order, into "multi-wavefront"
+// bins.  A bin is one workgroup of 4 or 8 wavefronts.  A cohort of at most 64
+// sessions never straddles a wavefront; a larger one starts on a wavefront
+// boundary and spans whole wavefronts; no cohort straddles a bin.  Each
+// wavefront has a 32-byte descriptor read with scalar loads.  The compaction
+// (stable partition, taken first) is a wavefront ballot + mbcnt rank; a
+// cohort spanning wavefronts adds an LDS exchange of per-wavefront popcounts
+// behind one workgroup barrier per step.
 //
-// Per-word update, branch-free.  With d the decision, r the route:
+// Route-table image in LDS.
+//   full:  row r < R holds the W masks table[r][w mod 16] * (w + 1); row R is
+//          zero.  No arithmetic is left for the masks.
+//   table: (when the full image would not fit) row r holds table[r][0..15],
+//          row R is zero; the masks are formed in registers with full-rate
+//          shifts and adds: the mask of w + 16 is the mask of w plus
+//          table[r][w mod 16] << 4 (exact modulo 2^32).
+// Block q (16 bytes) of row r is stored at block q ^ (r mod blocks-per-row)
+// to spread lanes reading different rows over the LDS banks.  After the rows
+// come the tool pairs (full image), the route thresholds and, in CDF mode, a
+// guide table: guide[b] is the route of outcome b * 2^(32-g), so the route
+// of o lies in [guide[o >> (32-g)], guide[(o >> (32-g)) + 1]] and a short
+// binary search of fixed trip count finishes it (the indexed-search guide
+// table of Chen and Asau, 1974).
+//
+// Per-word update, branch-free.  With d the decision and r the route:
 //   sh = d ? 0 : (31 - r) mod 32      rotl by (r+1) mod 32 == rotr by sh
-//   M  = d ? table[r][w mod 16]*(w+1) : 0     (row R of the LDS table is 0)
+//   M  = masks of row (d ? r : R)      (zero when not taken)
 //   oo = d ? 0 : o
 //   S' = (rotr(S, sh) ^ M) + oo       one v_alignbit_b32 + one v_xad_u32
-// For w >= 16 the mask is the one of w - 16 plus table[r][w mod 16] << 4
-// (exact modulo 2^32), one v_lshl_add_u32 per word instead of a multiply.
+//
+// Step schedule.  The decision of step t + 1 needs only word 0 after step
+// t, so it is made right after words 0..3 are updated; its popcount is
+// published and the workgroup barrier is passed there, the next mask row is
+// prefetched, and only then are the remaining words updated -- so the
+// barrier, the count exchange and the LDS latency overlap the bulk update.
+// The effects of step t are stored at the end of step t.
 
 #include <hip/hip_runtime.h>
 
@@ -48,7 +71,7 @@
 namespace {
 
 // ---------------------------------------------------------------------------
-// Device side
+// Device helpers
 // ---------------------------------------------------------------------------
 
 // MurmurHash3's 32-bit finalizer.
@@ -65,6 +88,52 @@ __device__ __forceinline__ uint32_t rotr32(uint32_t x, uint32_t s) {
     return __builtin_amdgcn_alignbit(x, x, s);  // uses s mod 32
 }
 
+// Hide a value's provenance from the optimizer so that the branch-free
+// update stays one alignbit + one xad per word (otherwise the select that
+// made `sh`/`oo` is pushed into every word).
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+    asm("" : "+v"(v));
+    return v;
+}
+
+// t * K for K = 1..16 from full-rate shifts and adds.  Every intermediate
+// passes through opaque(), so the optimizer cannot re-fuse the chain into a
+// quarter-rate v_mul_lo_u32.
+template <int K>
+__device__ __forceinline__ uint32_t mul_small(uint32_t t) {
+    static_assert(K >= 1 && K <= 16, "K");
+    if constexpr (K == 1) return opaque(t);
+    else if constexpr (K == 2 || K == 4 || K == 8 || K == 16) {
+        constexpr int s = K == 2 ? 1 : K == 4 ? 2 : K == 8 ? 3 : 4;
+        return opaque(t << s);
+    } else if constexpr (K == 3) return opaque((t << 1) + t);
+    else if constexpr (K == 5) return opaque((t << 2) + t);
+    else if constexpr (K == 9) return opaque((t << 3) + t);
+    else if constexpr (K == 6) return opaque(mul_small<3>(t) << 1);
+    else if constexpr (K == 7) return opaque((mul_small<3>(t) << 1) + t);
+    else if constexpr (K == 10) return opaque(mul_small<5>(t) << 1);
+    else if constexpr (K == 11) return opaque((mul_small<5>(t) << 1) + t);
+    else if constexpr (K == 12) return opaque(mul_small<3>(t) << 2);
+    else if constexpr (K == 13) return opaque((mul_small<3>(t) << 2) + t);
+    else if constexpr (K == 14) return opaque(mul_small<7>(t) << 1);
+    else return opaque((mul_small<7>(t) << 1) + t);  // 15
+}
+
+// A uniform value (kept in an SGPR) whose provenance is hidden.  Volatile,
+// so that address arithmetic derived from it is not hoisted out of the loop
+// it sits in, nor shared between two places that recompute it.
+__device__ __forceinline__ uint32_t opaque_s(uint32_t v) {
+    asm volatile("" : "+s"(v));
+    return v;
+}
+
+// `m` with a false data dependence on `after`: m cannot be formed before
+// `after` is.  Used to keep one band of masks live at a time.
+__device__ __forceinline__ uint32_t after_word(uint32_t m, uint32_t after) {
+    asm("" : "+v"(m) : "v"(after));
+    return m;
+}
+
 __device__ __forceinline__ uint32_t lane_rank(uint64_t m) {
     // number of set bits of m below this lane
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
@@ -73,6 +142,18 @@ __device__ __forceinline__ uint32_t lane_rank(uint64_t m) {
 
 __device__ __forceinline__ uint32_t uni(uint32_t v) {
     return __builtin_amdgcn_readfirstlane(v);
+}
+
+// Global accesses as a uniform base plus a 32-bit byte offset, so that they
+// compile to the scalar-base + 32-bit vector-offset form.
+__device__ __forceinline__ uint32_t ld32(const uint32_t* base, uint32_t byte_off) {
+    return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+__device__ __forceinline__ void st32(uint32_t* base, uint32_t byte_off, uint32_t v) {
+    *reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(base) + byte_off) = v;
+}
+__device__ __forceinline__ void st128(uint32_t* base, uint32_t byte_off, uint4 v) {
+    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(base) + byte_off) = v;
 }
 
 // Wavefront descriptor of the launch plan (8 x u32).
@@ -90,23 +171,42 @@ enum : uint32_t {
     WF_MULTI = 1u,    // this wavefront is part of a cohort of > 64 sessions
     WF_WGMULTI = 2u,  // some wavefront of the workgroup is (uniform per WG)
     // bits 8..15: index of this wavefront inside its cohort
-    // bits 16..23: wavefronts of the cohort
+    // bits 16..23: wavefronts of the cohort (at most 4)
     // bits 24..31: first wavefront (inside the workgroup) of the cohort
 };
 
 struct RouteArgs {
-    uint32_t mode;      // RC_ROUTE_MOD / RC_ROUTE_CDF
-    uint32_t n_routes;  // R
-    uint32_t pow2_mask; // R - 1 when R is a power of two, else 0
+    uint32_t mode;        // RC_ROUTE_MOD / RC_ROUTE_CDF
+    uint32_t n_routes;    // R
+    uint32_t pow2_mask;   // R - 1 when R is a power of two, else 0
     uint32_t is_pow2;
-    uint32_t cdf_n;     // R - 1 thresholds
-    uint32_t cdf_top;   // largest power of two <= cdf_n (0 if none)
+    uint32_t cdf_n;       // R - 1 thresholds
+    uint32_t cdf_top;     // largest power of two <= cdf_n (0 if none)
+    uint32_t guide_shift; // 32 - g (CDF mode)
+    uint32_t guide_top;   // largest step of the search inside a guide bucket
 };
 
-// Route key (MOD: o mod R; CDF: number of thresholds <= o, found by a
-// fixed-trip binary search over the LDS copy of the thresholds).
+// Route key from the LDS thresholds and guide table (see the file comment).
 __device__ __forceinline__ uint32_t route_of(uint32_t o, const RouteArgs& ra,
-                                             const uint32_t* cdf) {
+                                             const uint32_t* cdf, const uint32_t* guide) {
+    if (ra.mode == RC_ROUTE_MOD)
+        return ra.is_pow2 ? (o & ra.pow2_mask) : (o % ra.n_routes);
+    const uint32_t bkt = o >> ra.guide_shift;
+    uint32_t pos = guide[bkt];
+    const uint32_t hi = guide[bkt + 1u];
+    for (uint32_t stp = ra.guide_top; stp != 0u; stp >>= 1) {
+        const uint32_t i = pos + stp;
+        const uint32_t j = i <= hi ? i : hi;
+        const uint32_t v = cdf[j == 0u ? 0u : j - 1u];
+        pos = (i <= hi && v <= o) ? i : pos;
+    }
+    return pos;
+}
+
+// Route key by a plain fixed-trip binary search over all thresholds (used by
+// the host-round-trip body kernel, which has no guide table).
+__device__ __forceinline__ uint32_t route_of_bsearch(uint32_t o, const RouteArgs& ra,
+                                                     const uint32_t* cdf) {
     if (ra.mode == RC_ROUTE_MOD)
         return ra.is_pow2 ? (o & ra.pow2_mask) : (o % ra.n_routes);
     uint32_t pos = 0;
@@ -117,24 +217,6 @@ __device__ __forceinline__ uint32_t route_of(uint32_t o, const RouteArgs& ra,
     }
     return pos;
 }
-
-struct ChainArgs {
-    uint32_t* state;
-    uint32_t* outcome;
-    uint32_t* eff_sid;
-    uint32_t* eff_tool;
-    uint32_t* eff_payload;
-    uint32_t* n_taken;
-    const uint32_t* tab;      // (R+1) x 16 swizzled rows, row R all zero
-    const uint32_t* tools;    // [R] (table[r][0] & 7) | (table[r][1] & 7) << 8
-    const uint32_t* cdf;      // [R-1]
-    const uint32_t* offsets;  // [C+1]
-    const uint32_t* wdesc;    // [bins][waves][WD_WORDS]
-    RouteArgs ra;
-    uint32_t ld, n_words, n_cohorts, thr, step0, n_steps;
-    uint32_t cohort_begin, cohort_end, bin_lo, bin_hi;
-    uint32_t lds_tools_off, lds_cdf_off, lds_cnt_off;  // in words
-};
 
 // Per-lane view of the plan for one bin.
 struct LaneCohort {
@@ -185,153 +267,362 @@ __device__ __forceinline__ LaneCohort lane_cohort(const uint32_t* __restrict__ w
     return L;
 }
 
-// Stable-partition slot of this lane at one step.  Returns the slot; n1 gets
-// the cohort's taken count.  `par` toggles once per workgroup barrier.
-template <int NWAVE>
-__device__ __forceinline__ uint32_t compact_slot(const LaneCohort& L, bool dk, uint32_t lane,
-                                                 uint32_t wv, uint32_t* cnt_lds,
-                                                 uint32_t& par, uint32_t& n1) {
-    const uint64_t bal = __ballot(dk);
+// Publish this wavefront's popcount (multi-wavefront cohorts), pass the
+// workgroup barrier, read the cohort's per-wavefront counts (cnt[wf .. wf+3];
+// only the first nw belong to the cohort).  Called only in workgroups that
+// hold a multi-wavefront cohort, the same number of times by every
+// wavefront.  Publication k goes to buffer k mod 2: its readers finish
+// before the barrier that follows publication k + 1, which precedes any
+// write of publication k + 2.
+__device__ __forceinline__ void exchange_counts(const LaneCohort& L, uint64_t bal, uint32_t lane,
+                                                uint32_t wv, uint32_t* cnt_lds, uint32_t cnt_stride,
+                                                uint32_t& pub, uint32_t (&c4)[4]) {
+    uint32_t* buf = cnt_lds + (pub & 1u) * cnt_stride;
+    if ((L.flags & WF_MULTI) && lane == 0u) buf[wv] = (uint32_t)__popcll(bal);
+    __syncthreads();
+    if (L.flags & WF_MULTI) {
+        const uint32_t wf = L.flags >> 24;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c4[i] = uni(buf[wf + i]);  // uniform: keep in SGPRs
+    }
+    pub += 1u;
+}
+
+// Stable-partition slot of this lane for a step with ballot `bal`; c4 holds
+// the cohort's per-wavefront counts of that step (multi-wavefront cohorts).
+__device__ __forceinline__ uint32_t slot_of(const LaneCohort& L, bool dk, uint64_t bal,
+                                            const uint32_t (&c4)[4], uint32_t& n1) {
     uint32_t rank_t;
     if (!(L.flags & WF_MULTI)) {
         const uint64_t bs = bal & L.seg;
         n1 = (uint32_t)__popcll(bs);
         rank_t = lane_rank(bs);
     } else {
-        n1 = 0;
-        rank_t = 0;
-    }
-    if (L.flags & WF_WGMULTI) {
-        uint32_t* cnt = cnt_lds + par * NWAVE;
-        if ((L.flags & WF_MULTI) && lane == 0u)
-            cnt[wv] = (uint32_t)__popcll(bal);
-        __syncthreads();
-        if (L.flags & WF_MULTI) {
-            const uint32_t wi = (L.flags >> 8) & 0xFFu;
-            const uint32_t nw = (L.flags >> 16) & 0xFFu;
-            const uint32_t wf = L.flags >> 24;
-            uint32_t before = 0, total = 0;
-            for (uint32_t i = 0; i < nw; ++i) {
-                const uint32_t ci = cnt[wf + i];
-                total += ci;
-                before += (i < wi) ? ci : 0u;
-            }
-            n1 = total;
-            rank_t = before + lane_rank(bal);
+        const uint32_t wi = (L.flags >> 8) & 0xFFu;
+        const uint32_t nw = (L.flags >> 16) & 0xFFu;
+        uint32_t before = 0, total = 0;
+#pragma unroll
+        for (uint32_t i = 0; i < 4; ++i) {
+            total += (i < nw) ? c4[i] : 0u;
+            before += (i < wi) ? c4[i] : 0u;
         }
-        par ^= 1u;
+        n1 = total;
+        rank_t = before + lane_rank(bal);
     }
     const uint32_t in_c = L.s - L.b;
     return L.b + (dk ? rank_t : n1 + (in_c - rank_t));
 }
 
-// Load one table row (16 words, 4 swizzled 16-byte blocks) from LDS.
-__device__ __forceinline__ void load_row(const uint32_t* lds_tab, uint32_t row, uint32_t (&tw)[16]) {
-    const uint4* r4 = reinterpret_cast<const uint4*>(lds_tab) + row * 4u;
+// ---------------------------------------------------------------------------
+// Table image (built once per handle)
+// ---------------------------------------------------------------------------
+struct ImageArgs {
+    const uint32_t* raw;  // [R][16]
+    const uint32_t* cdf;  // [R-1]
+    uint32_t* img;
+    uint32_t* max_span;   // out: largest guide bucket span
+    uint32_t n_routes, row_words, full, tab_words, tools_off, cdf_off, cdf_n;
+    uint32_t guide_off, guide_n, guide_shift, total_words;
+};
+
+// number of thresholds <= x (plain binary search over global memory)
+__device__ __forceinline__ uint32_t count_le(const uint32_t* cdf, uint32_t n, uint32_t x) {
+    uint32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const uint32_t mid = lo + (hi - lo) / 2u;
+        if (cdf[mid] <= x) lo = mid + 1u; else hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(256) void rc_prep_kernel(ImageArgs a) {
+    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+    if (i >= a.total_words) return;
+    const uint32_t R = a.n_routes;
+    uint32_t v = 0;
+    if (i < a.tab_words) {
+        const uint32_t WM = a.row_words, NB = WM / 4u;
+        const uint32_t r = i / WM, p = i % WM;
+        const uint32_t q = (p >> 2) ^ (r & (NB - 1u));
+        const uint32_t w = 4u * q + (p & 3u);
+        if (r < R) v = a.full ? a.raw[r * 16u + (w & 15u)] * (w + 1u) : a.raw[r * 16u + w];
+    } else if (a.full && i >= a.tools_off && i < a.tools_off + R) {
+        const uint32_t r = i - a.tools_off;
+        v = (a.raw[r * 16u] & 7u) | ((a.raw[r * 16u + 1u] & 7u) << 8);
+    } else if (i >= a.cdf_off && i < a.cdf_off + a.cdf_n) {
+        v = a.cdf[i - a.cdf_off];
+    } else if (a.guide_n && i >= a.guide_off && i < a.guide_off + a.guide_n) {
+        const uint32_t bkt = i - a.guide_off;
+        const uint32_t last = a.guide_n - 1u;
+        v = bkt == last ? a.cdf_n : count_le(a.cdf, a.cdf_n, bkt << a.guide_shift);
+        if (bkt < last) {
+            const uint32_t nxt = bkt + 1u == last ? a.cdf_n
+                                                  : count_le(a.cdf, a.cdf_n, (bkt + 1u) << a.guide_shift);
+            atomicMax(a.max_span, nxt - v);
+        }
+    }
+    a.img[i] = v;
+}
+
+// ---------------------------------------------------------------------------
+// Device-resident chain
+// ---------------------------------------------------------------------------
+struct ChainArgs {
+    uint32_t* state;
+    uint32_t* outcome;
+    uint32_t* eff_sid;
+    uint32_t* eff_tool;
+    uint32_t* eff_payload;
+    uint32_t* n_taken;
+    const uint32_t* img;      // LDS image, img_words words
+    const uint32_t* offsets;  // [C+1]
+    const uint32_t* wdesc;    // [bins][waves][WD_WORDS]
+    RouteArgs ra;
+    uint32_t ld, n_words, n_cohorts, thr, step0, n_steps;
+    uint32_t cohort_begin, cohort_end;
+    uint32_t bins_a_lo, bins_a_n, bins_b_lo, bins_b_n;  // sub-wave / multi-wave bins
+    uint32_t img_words, tools_off, cdf_off, guide_off;  // in words
+};
+
+// One row (WM words) of the image; logical block q of row r sits at block
+// q ^ (r mod NB), so its byte address is one XOR away.
+template <int WM>
+__device__ __forceinline__ void load_row(const uint32_t* lds, uint32_t row, uint32_t (&m)[WM]) {
+    constexpr uint32_t NB = WM / 4;
+    const uint32_t rb = row * (NB * 16u) + ((row & (NB - 1u)) << 4);
+    const char* base = reinterpret_cast<const char*>(lds);
 #pragma unroll
-    for (uint32_t q = 0; q < 4; ++q) {
-        const uint4 v = r4[(q + row) & 3u];
-        tw[4 * q + 0] = v.x;
-        tw[4 * q + 1] = v.y;
-        tw[4 * q + 2] = v.z;
-        tw[4 * q + 3] = v.w;
+    for (uint32_t q = 0; q < NB; ++q) {
+        const uint4 v = *reinterpret_cast<const uint4*>(base + (rb ^ (q << 4)));
+        m[4 * q + 0] = v.x;
+        m[4 * q + 1] = v.y;
+        m[4 * q + 2] = v.z;
+        m[4 * q + 3] = v.w;
     }
 }
 
-template <int NWAVE>
-__device__ __forceinline__ void stage_tables(uint32_t* lds, const ChainArgs& a, uint32_t tid) {
-    constexpr uint32_t WG = NWAVE * 64;
-    const uint32_t n4 = (a.ra.n_routes + 1u) * 4u;  // uint4 per table
-    const uint4* src = reinterpret_cast<const uint4*>(a.tab);
-    uint4* dst = reinterpret_cast<uint4*>(lds);
-    for (uint32_t i = tid; i < n4; i += WG) dst[i] = src[i];
-    for (uint32_t i = tid; i < a.ra.n_routes; i += WG) lds[a.lds_tools_off + i] = a.tools[i];
-    if (a.ra.mode == RC_ROUTE_CDF)
-        for (uint32_t i = tid; i < a.ra.cdf_n; i += WG) lds[a.lds_cdf_off + i] = a.cdf[i];
+// Tool of route r for decision d: table[r][d] mod 8.
+template <bool FULL>
+__device__ __forceinline__ uint32_t tool_of(const uint32_t* lds, const uint32_t* lds_tools,
+                                            uint32_t r, bool d) {
+    if constexpr (FULL) {
+        return (lds_tools[r] >> (d ? 8u : 0u)) & 7u;
+    } else {
+        // table[r][0..3] is block 0 of row r, stored at block (r mod 4)
+        return lds[r * 16u + ((r & 3u) << 2) + (d ? 1u : 0u)] & 7u;
+    }
 }
 
-// Device-resident chain: T steps per bin without leaving the kernel.
-template <int WMAX, bool EXACT, int NWAVE>
-__global__ __launch_bounds__(NWAVE * 64) void rc_chain_kernel(ChainArgs a) {
+// Table image, band 0 (words 4..15): masks table[r][j] * (j + 1).
+template <int J, bool EXACT, int WMAX>
+__device__ __forceinline__ void band0(uint32_t (&S)[WMAX], const uint32_t (&tv)[16],
+                                      uint32_t (&M)[16], uint32_t sh, uint32_t oo, uint32_t W) {
+    if constexpr (J < 16) {
+        M[J] = mul_small<J + 1>(tv[J]);
+        if (J < WMAX && (EXACT || (uint32_t)J < W)) S[J < WMAX ? J : 0] = (rotr32(S[J < WMAX ? J : 0], sh) ^ M[J]) + oo;
+        band0<J + 1, EXACT, WMAX>(S, tv, M, sh, oo, W);
+    }
+}
+
+// Table image, band B >= 1 (words 16 B .. 16 B + 15): the mask of w is the
+// mask of w - 16 plus table[r][w mod 16] << 4.
+template <int B, bool EXACT, int WMAX>
+__device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[16],
+                                     uint32_t (&M)[16], uint32_t sh, uint32_t oo, uint32_t W) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        constexpr int base = 16 * B;
+        M[j] = after_word((tv[j] << 4) + M[j], S[base + j - 16]);
+        if (EXACT || (uint32_t)(base + j) < W) S[base + j] = (rotr32(S[base + j], sh) ^ M[j]) + oo;
+    }
+}
+
+template <int WMAX, bool EXACT, int NWAVE, bool FULL>
+struct Chain {
+    static constexpr int MW = FULL ? WMAX : 16;
+    static constexpr uint32_t CNT_STRIDE = NWAVE + 4;
+
+    // Everything one lane carries from step to step.
+    struct Lane {
+        uint32_t S[WMAX];
+        uint32_t o, r, step, pub;
+        bool dk;
+        uint64_t bal;
+        uint32_t c4[4];
+    };
+
+    // One chained step.  Full image: `mc` holds this step's masks and the
+    // next step's row is prefetched into `mn`.  Table image: `mc` receives
+    // this step's table row.
+    static __device__ __forceinline__ void step(const ChainArgs& a, const LaneCohort& L, Lane& st,
+                                                uint32_t t, uint32_t lane, uint32_t wv,
+                                                const uint32_t* lds, uint32_t* lds_cnt,
+                                                uint32_t (&mc)[MW], uint32_t (&mn)[MW]) {
+        const uint32_t R = a.ra.n_routes;
+        const uint32_t W = a.n_words;
+        const bool wgm = (L.flags & WF_WGMULTI) != 0u;
+        const bool has_next = t + 1u < a.n_steps;
+
+        const uint32_t sh = opaque(st.dk ? 0u : ((31u - st.r) & 31u));
+        const uint32_t oo = opaque(st.dk ? 0u : st.o);
+        const uint32_t tool = tool_of<FULL>(lds, lds + a.tools_off, st.r, st.dk);
+        uint32_t M[16];  // table image: running masks of the 16 columns
+        if constexpr (!FULL) {
+            load_row<16>(lds, st.dk ? st.r : R, mc);
+            M[0] = mul_small<1>(mc[0]);
+            M[1] = mul_small<2>(mc[1]);
+            M[2] = mul_small<3>(mc[2]);
+            M[3] = mul_small<4>(mc[3]);
+        }
+
+        // (a6) words 0..3: the payload, and the input of the next decision
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t m = FULL ? mc[w] : M[w];
+            if (EXACT || (uint32_t)w < W) st.S[w] = (rotr32(st.S[w], sh) ^ m) + oo;
+        }
+
+        // (a8) chain: next outcome; (a3, a4) the next step's route and decision
+        const uint32_t o_n = dev_fmix32(st.S[0]);
+        uint32_t r_n = 0;
+        bool d_n = false;
+        uint64_t bal_n = 0;
+        uint32_t c4n[4] = {0u, 0u, 0u, 0u};
+        if (has_next) {
+            r_n = route_of(o_n, a.ra, lds + a.cdf_off, lds + a.guide_off);
+            d_n = L.active && ((dev_fmix32(st.S[0] ^ o_n ^ (st.step + 1u)) & 0xFFFFu) < a.thr);
+            bal_n = __ballot(d_n);
+            if (wgm) exchange_counts(L, bal_n, lane, wv, lds_cnt, CNT_STRIDE, st.pub, c4n);
+            if constexpr (FULL) load_row<MW>(lds, d_n ? r_n : R, mn);
+        }
+
+        // (a6) the remaining words
+        if constexpr (FULL) {
+#pragma unroll
+            for (int w = 4; w < WMAX; ++w)
+                if (EXACT || (uint32_t)w < W) st.S[w] = (rotr32(st.S[w], sh) ^ mc[w]) + oo;
+        } else {
+            // band by band; a scheduling fence between bands keeps only one
+            // band's masks live
+            band0<4, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (WMAX > 16) {
+                band<1, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if constexpr (WMAX > 32) {
+                band<2, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
+                __builtin_amdgcn_sched_barrier(0);
+                band<3, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
+            }
+        }
+
+        // (a5) compaction of this step; (a7) emit.  slot - b < k always holds;
+        // the test keeps a compaction defect from ever becoming a write outside
+        // the cohort's slots.
+        uint32_t n1;
+        const uint32_t slot = slot_of(L, st.dk, st.bal, st.c4, n1);
+        if (L.active && slot - L.b < L.k) {
+            const size_t slice = (size_t)t * a.ld;
+            st32(a.eff_sid + slice, slot << 2, L.s);
+            st32(a.eff_tool + slice, slot << 2, tool);
+            st128(a.eff_payload + slice * 4u, slot << 4,
+                  make_uint4(st.S[0], st.S[1], st.S[2], st.S[3]));
+            if (L.s == L.b) st32(a.n_taken + (size_t)t * a.n_cohorts, L.c << 2, n1);
+        }
+
+        st.o = o_n;
+        st.r = r_n;
+        st.dk = d_n;
+        st.bal = bal_n;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) st.c4[i] = c4n[i];
+        st.step += 1u;
+    }
+};
+
+// The table-image variant runs two 512-lane workgroups per CU, so it is held
+// to four wavefronts per SIMD (128 VGPRs).
+template <int WMAX, bool EXACT, int NWAVE, bool FULL>
+__global__ __launch_bounds__(NWAVE * 64, FULL ? 1 : 4) void rc_chain_kernel(ChainArgs a) {
+    using C = Chain<WMAX, EXACT, NWAVE, FULL>;
+    constexpr int MW = C::MW;
     extern __shared__ uint4 lds4[];
     uint32_t* lds = reinterpret_cast<uint32_t*>(lds4);
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
     const uint32_t wv = tid >> 6;
     const uint32_t W = a.n_words;
-    const size_t ld = a.ld;
+    const uint32_t R = a.ra.n_routes;
+    const uint32_t T = a.n_steps;
 
-    stage_tables<NWAVE>(lds, a, tid);
+    // (a1) stage the table image once per workgroup
+    {
+        const uint4* src = reinterpret_cast<const uint4*>(a.img);
+        for (uint32_t i = tid; i < a.img_words / 4u; i += NWAVE * 64) lds4[i] = src[i];
+    }
     __syncthreads();
-    const uint32_t* lds_tools = lds + a.lds_tools_off;
-    const uint32_t* lds_cdf = lds + a.lds_cdf_off;
-    uint32_t* lds_cnt = lds + a.lds_cnt_off;
-    uint32_t par = 0;
+    uint32_t* lds_cnt = lds + a.img_words;  // [2][NWAVE + 4]
+    const uint32_t n_bins = a.bins_a_n + a.bins_b_n;
+    typename C::Lane st;
+    st.pub = 0;
 
-    for (uint32_t bin = a.bin_lo + blockIdx.x; bin < a.bin_hi; bin += gridDim.x) {
+    for (uint32_t i = blockIdx.x; i < n_bins; i += gridDim.x) {
+        const uint32_t bin = i < a.bins_a_n ? a.bins_a_lo + i : a.bins_b_lo + (i - a.bins_a_n);
         const LaneCohort L = lane_cohort(a.wdesc + ((size_t)bin * NWAVE + wv) * WD_WORDS,
                                          a.offsets, lane, a.cohort_begin, a.cohort_end);
-        uint32_t S[WMAX];
-        uint32_t o = 0;
+        const bool wgm = (L.flags & WF_WGMULTI) != 0u;
+        const uint32_t soff = L.s << 2;
+
+        // (a2) load the state words and the pending outcome
 #pragma unroll
-        for (int w = 0; w < WMAX; ++w) S[w] = 0;
+        for (int w = 0; w < WMAX; ++w) st.S[w] = 0;
+        st.o = 0;
         if (L.active) {
+            const uint32_t ldw = opaque_s(a.ld);
 #pragma unroll
             for (int w = 0; w < WMAX; ++w)
-                if (EXACT || (uint32_t)w < W) S[w] = a.state[(size_t)w * ld + L.s];
-            o = a.outcome[L.s];
+                if (EXACT || (uint32_t)w < W) st.S[w] = ld32(a.state + (size_t)w * ldw, soff);
+            st.o = ld32(a.outcome, soff);
         }
 
-        for (uint32_t t = 0; t < a.n_steps; ++t) {
-            const uint32_t step = a.step0 + t;
-            const uint32_t r = route_of(o, a.ra, lds_cdf);
-            const uint32_t h = dev_fmix32(S[0] ^ o ^ step);
-            const bool dk = L.active && ((h & 0xFFFFu) < a.thr);
-            uint32_t n1;
-            const uint32_t slot = compact_slot<NWAVE>(L, dk, lane, wv, lds_cnt, par, n1);
+        // decision of the first step
+        st.step = a.step0;
+        st.r = route_of(st.o, a.ra, lds + a.cdf_off, lds + a.guide_off);
+        st.dk = L.active && ((dev_fmix32(st.S[0] ^ st.o ^ st.step) & 0xFFFFu) < a.thr);
+        st.bal = __ballot(st.dk);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) st.c4[k] = 0u;
+        if (wgm) exchange_counts(L, st.bal, lane, wv, lds_cnt, C::CNT_STRIDE, st.pub, st.c4);
+        uint32_t mA[MW], mB[MW];
+        if constexpr (FULL) load_row<MW>(lds, st.dk ? st.r : R, mA);
 
-            const uint32_t row = dk ? r : a.ra.n_routes;
-            const uint32_t sh = dk ? 0u : ((31u - r) & 31u);
-            const uint32_t oo = dk ? 0u : o;
-            uint32_t tw[16];
-            load_row(lds, row, tw);
-            uint32_t M[16];
-#pragma unroll
-            for (int j = 0; j < 16; ++j) M[j] = tw[j] * (uint32_t)(j + 1);
-#pragma unroll
-            for (int w = 0; w < WMAX; ++w) {
-                const int j = w & 15;
-                if (w >= 16) M[j] += tw[j] << 4;
-                if (EXACT || (uint32_t)w < W) S[w] = (rotr32(S[w], sh) ^ M[j]) + oo;
-            }
-            const uint32_t tool = (lds_tools[r] >> (dk ? 8u : 0u)) & 7u;
-
-            // slot - b < k always holds; the test keeps a compaction defect
-            // from ever turning into a write outside the cohort's slots
-            if (L.active && slot - L.b < L.k) {
-                const size_t e = (size_t)t * ld + slot;
-                a.eff_sid[e] = L.s;
-                a.eff_tool[e] = tool;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) a.eff_payload[((size_t)t * 4 + q) * ld + slot] = S[q];
-                if (L.s == L.b) a.n_taken[(size_t)t * a.n_cohorts + L.c] = n1;
-            }
-            o = dev_fmix32(S[0]);
+        // T chained steps, unrolled by two so the prefetched row needs no copy
+        for (uint32_t t = 0; t < T; t += 2u) {
+            C::step(a, L, st, t, lane, wv, lds, lds_cnt, mA, mB);
+            if (t + 1u < T) C::step(a, L, st, t + 1u, lane, wv, lds, lds_cnt, mB, mA);
         }
 
+        // (a9) store the state and the next outcome (addresses recomputed
+        // rather than kept live across the chain)
         if (L.active) {
+            const uint32_t ldw = opaque_s(a.ld);
 #pragma unroll
             for (int w = 0; w < WMAX; ++w)
-                if (EXACT || (uint32_t)w < W) a.state[(size_t)w * ld + L.s] = S[w];
-            a.outcome[L.s] = o;
+                if (EXACT || (uint32_t)w < W) st32(a.state + (size_t)w * ldw, soff, st.S[w]);
+            st32(a.outcome, soff, st.o);
         }
     }
 }
 
-// Host round trip, part 1: decide and compact one step.  Writes n_taken,
-// appends (sid, slot) to the taken or not-taken list, and counts both
-// populations in ctr[parity][0..1] (ctr[parity][0] is the 4-byte word the
-// host reads).  Block 0 clears the other parity's counters for the next step.
+// ---------------------------------------------------------------------------
+// Host round trip
+// ---------------------------------------------------------------------------
+
+// Part 1: decide and compact one step.  Writes n_taken, appends (sid, slot)
+// to the taken or not-taken list, and counts both populations in
+// ctr[parity][0..1] (ctr[parity][0] is the 4-byte word the host reads).
+// Block 0 clears the other parity's counters for the next step.
 struct DecideArgs {
     const uint32_t* state;
     const uint32_t* outcome;
@@ -342,49 +633,54 @@ struct DecideArgs {
     const uint32_t* offsets;
     const uint32_t* wdesc;
     uint32_t thr, step, t_index, n_cohorts, n_sessions;
-    uint32_t cohort_begin, cohort_end, bin_lo, bin_hi, parity;
+    uint32_t cohort_begin, cohort_end;
+    uint32_t bins_a_lo, bins_a_n, bins_b_lo, bins_b_n, parity;
 };
 
 template <int NWAVE>
 __global__ __launch_bounds__(NWAVE * 64) void rc_decide_kernel(DecideArgs a) {
-    __shared__ uint32_t cnt_lds[2 * NWAVE];
+    __shared__ uint32_t cnt_lds[2 * (NWAVE + 4)];
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
     const uint32_t wv = tid >> 6;
-    uint32_t par = 0;
     if (blockIdx.x == 0 && tid == 0) {
         a.ctr[(a.parity ^ 1u) * 2u + 0u] = 0u;
         a.ctr[(a.parity ^ 1u) * 2u + 1u] = 0u;
     }
-    for (uint32_t bin = a.bin_lo + blockIdx.x; bin < a.bin_hi; bin += gridDim.x) {
+    uint32_t pub = 0;
+    const uint32_t n_bins = a.bins_a_n + a.bins_b_n;
+    for (uint32_t i = blockIdx.x; i < n_bins; i += gridDim.x) {
+        const uint32_t bin = i < a.bins_a_n ? a.bins_a_lo + i : a.bins_b_lo + (i - a.bins_a_n);
         const LaneCohort L = lane_cohort(a.wdesc + ((size_t)bin * NWAVE + wv) * WD_WORDS,
                                          a.offsets, lane, a.cohort_begin, a.cohort_end);
         uint32_t s0w = 0, o = 0;
         if (L.active) {
-            s0w = a.state[L.s];
-            o = a.outcome[L.s];
+            s0w = ld32(a.state, L.s << 2);
+            o = ld32(a.outcome, L.s << 2);
         }
         const bool dk = L.active && ((dev_fmix32(s0w ^ o ^ a.step) & 0xFFFFu) < a.thr);
+        const uint64_t bal = __ballot(dk);
+        uint32_t c4[4] = {0u, 0u, 0u, 0u};
+        if (L.flags & WF_WGMULTI) exchange_counts(L, bal, lane, wv, cnt_lds, NWAVE + 4, pub, c4);
         uint32_t n1;
-        const uint32_t slot = compact_slot<NWAVE>(L, dk, lane, wv, cnt_lds, par, n1);
+        const uint32_t slot = slot_of(L, dk, bal, c4, n1);
         if (L.active && L.s == L.b) a.n_taken[(size_t)a.t_index * a.n_cohorts + L.c] = n1;
 
-        const uint64_t bt = __ballot(dk);
         const uint64_t bn = __ballot(L.active && !dk);
         uint32_t base_t = 0, base_n = 0;
         if (lane == 0u) {
-            if (bt) base_t = atomicAdd(&a.ctr[a.parity * 2u + 0u], (uint32_t)__popcll(bt));
+            if (bal) base_t = atomicAdd(&a.ctr[a.parity * 2u + 0u], (uint32_t)__popcll(bal));
             if (bn) base_n = atomicAdd(&a.ctr[a.parity * 2u + 1u], (uint32_t)__popcll(bn));
         }
         base_t = uni(base_t);
         base_n = uni(base_n);
-        const uint32_t at = dk ? base_t + lane_rank(bt) : base_n + lane_rank(bn);
+        const uint32_t at = dk ? base_t + lane_rank(bal) : base_n + lane_rank(bn);
         if (L.active && at < a.n_sessions && slot - L.b < L.k)
             (dk ? a.list_taken : a.list_not)[at] = make_uint2(L.s, slot);
     }
 }
 
-// Host round trip, part 2: the route body the host selected, over its list.
+// Part 2: the route body the host selected, over its compacted list.
 struct BodyArgs {
     uint32_t* state;
     uint32_t* outcome;
@@ -392,8 +688,7 @@ struct BodyArgs {
     uint32_t* eff_tool;
     uint32_t* eff_payload;
     const uint2* list;
-    const uint32_t* tab;
-    const uint32_t* tools;
+    const uint32_t* raw;   // [R][16]
     const uint32_t* cdf;
     RouteArgs ra;
     uint32_t ld, n_words, count, t_index, n_sessions;
@@ -410,29 +705,20 @@ __global__ __launch_bounds__(256) void rc_body_kernel(BodyArgs a) {
     const uint32_t i = blockIdx.x * 256u + tid;
     if (i >= a.count) return;
     const uint32_t W = a.n_words;
-    const size_t ld = a.ld;
     const uint2 e = a.list[i];
     const uint32_t s = e.x, slot = e.y;
     if (s >= a.n_sessions || slot >= a.n_sessions) return;  // never taken by valid lists
-    const uint32_t o = a.outcome[s];
-    const uint32_t r = route_of(o, a.ra, cdf_lds);
+    const uint32_t soff = s << 2;
+    const uint32_t o = ld32(a.outcome, soff);
+    const uint32_t r = route_of_bsearch(o, a.ra, cdf_lds);
     uint32_t S[WMAX];
 #pragma unroll
     for (int w = 0; w < WMAX; ++w)
-        S[w] = (EXACT || (uint32_t)w < W) ? a.state[(size_t)w * ld + s] : 0u;
+        S[w] = (EXACT || (uint32_t)w < W) ? ld32(a.state + (size_t)w * a.ld, soff) : 0u;
     if (TAKEN) {
-        uint32_t tw[16];
-        const uint4* r4 = reinterpret_cast<const uint4*>(a.tab) + r * 4u;
+        const uint32_t* row = a.raw + r * 16u;
 #pragma unroll
-        for (uint32_t q = 0; q < 4; ++q) {
-            const uint4 v = r4[(q + r) & 3u];
-            tw[4 * q + 0] = v.x;
-            tw[4 * q + 1] = v.y;
-            tw[4 * q + 2] = v.z;
-            tw[4 * q + 3] = v.w;
-        }
-#pragma unroll
-        for (int w = 0; w < WMAX; ++w) S[w] ^= tw[w & 15] * (uint32_t)(w + 1);
+        for (int w = 0; w < WMAX; ++w) S[w] ^= row[w & 15] * (uint32_t)(w + 1);
     } else {
         const uint32_t sh = (31u - r) & 31u;
 #pragma unroll
@@ -440,13 +726,12 @@ __global__ __launch_bounds__(256) void rc_body_kernel(BodyArgs a) {
     }
 #pragma unroll
     for (int w = 0; w < WMAX; ++w)
-        if (EXACT || (uint32_t)w < W) a.state[(size_t)w * ld + s] = S[w];
-    const size_t eo = (size_t)a.t_index * ld + slot;
-    a.eff_sid[eo] = s;
-    a.eff_tool[eo] = (a.tools[r] >> (TAKEN ? 8u : 0u)) & 7u;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) a.eff_payload[((size_t)a.t_index * 4 + q) * ld + slot] = S[q];
-    a.outcome[s] = dev_fmix32(S[0]);
+        if (EXACT || (uint32_t)w < W) st32(a.state + (size_t)w * a.ld, soff, S[w]);
+    const size_t slice = (size_t)a.t_index * a.ld;
+    st32(a.eff_sid + slice, slot << 2, s);
+    st32(a.eff_tool + slice, slot << 2, (a.raw[r * 16u + (TAKEN ? 1u : 0u)]) & 7u);
+    st128(a.eff_payload + slice * 4u, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
+    st32(a.outcome, soff, dev_fmix32(S[0]));
 }
 
 // ---------------------------------------------------------------------------
@@ -458,17 +743,21 @@ typedef void (*DecideFn)(DecideArgs);
 typedef void (*BodyFn)(BodyArgs);
 
 template <int WMAX, bool EXACT>
-ChainFn chain_fn(uint32_t nwave) {
-    return nwave == 8 ? rc_chain_kernel<WMAX, EXACT, 8> : rc_chain_kernel<WMAX, EXACT, 4>;
+ChainFn chain_fn(uint32_t nwave, bool full) {
+    if (!full) {
+        if constexpr (WMAX >= 32) return rc_chain_kernel<WMAX, EXACT, 8, false>;
+        return nullptr;
+    }
+    return nwave == 8 ? rc_chain_kernel<WMAX, EXACT, 8, true> : rc_chain_kernel<WMAX, EXACT, 4, true>;
 }
 
-ChainFn pick_chain(uint32_t wmax, bool exact, uint32_t nwave) {
+ChainFn pick_chain(uint32_t wmax, bool exact, uint32_t nwave, bool full) {
     switch (wmax) {
-        case 4: return exact ? chain_fn<4, true>(nwave) : chain_fn<4, false>(nwave);
-        case 8: return exact ? chain_fn<8, true>(nwave) : chain_fn<8, false>(nwave);
-        case 16: return exact ? chain_fn<16, true>(nwave) : chain_fn<16, false>(nwave);
-        case 32: return exact ? chain_fn<32, true>(nwave) : chain_fn<32, false>(nwave);
-        default: return exact ? chain_fn<64, true>(nwave) : chain_fn<64, false>(nwave);
+        case 4: return exact ? chain_fn<4, true>(nwave, full) : chain_fn<4, false>(nwave, full);
+        case 8: return exact ? chain_fn<8, true>(nwave, full) : chain_fn<8, false>(nwave, full);
+        case 16: return exact ? chain_fn<16, true>(nwave, full) : chain_fn<16, false>(nwave, full);
+        case 32: return exact ? chain_fn<32, true>(nwave, full) : chain_fn<32, false>(nwave, full);
+        default: return exact ? chain_fn<64, true>(nwave, full) : chain_fn<64, false>(nwave, full);
     }
 }
 
@@ -511,6 +800,26 @@ uint32_t next_pow2_words(uint32_t w) {
     return p;
 }
 
+uint32_t ceil_log2(uint32_t x) {
+    uint32_t g = 0;
+    while ((1u << g) < x) ++g;
+    return g;
+}
+
+// The launch plan: per-wavefront descriptors plus the lookups that turn a
+// cohort range into bin ranges.  Built on the host, without a device.
+struct Plan {
+    uint32_t nwave = 4;
+    uint32_t n_bins = 0, n_bins_a = 0, idle_lanes = 0;
+    std::vector<uint32_t> wdesc;             // [bins][nwave][WD_WORDS]
+    std::vector<uint32_t> bin_of_cohort;     // [C]
+    std::vector<uint32_t> first_a, first_b;  // [C+1]: first cohort >= c of the class (C if none)
+    std::vector<int32_t> last_a, last_b;     // [C]: last cohort <= c of the class (-1 if none)
+};
+
+constexpr size_t FULL_IMAGE_LIMIT = 72u * 1024u;  // bytes of the full mask image
+constexpr size_t LDS_TWO_PER_CU = 80u * 1024u;    // two workgroups per CU fit below this
+
 }  // namespace
 
 struct rc_cohort {
@@ -519,18 +828,17 @@ struct rc_cohort {
     RouteArgs ra{};
     uint32_t wmax = 4;
     bool exact = true;
+    bool full = true;
     uint32_t nwave = 4;
-    uint32_t n_bins = 0;
-    uint32_t idle_lanes = 0;
-    uint32_t max_grid = 1;
+    uint32_t img_words = 0, tools_off = 0, cdf_off = 0, guide_off = 0;
     size_t chain_lds_bytes = 0;
-    uint32_t lds_tools_off = 0, lds_cdf_off = 0, lds_cnt_off = 0;
-    std::vector<uint32_t> offsets;        // host copy [C+1]
-    std::vector<uint32_t> bin_of_cohort;  // [C]
+    std::vector<uint32_t> offsets;  // host copy [C+1]
+    Plan plan;
     uint32_t* d_offsets = nullptr;
-    uint32_t* d_tab = nullptr;
-    uint32_t* d_tools = nullptr;
+    uint32_t* d_raw = nullptr;
     uint32_t* d_cdf = nullptr;
+    uint32_t* d_img = nullptr;
+    uint32_t* d_span = nullptr;
     uint32_t* d_wdesc = nullptr;
     uint2* d_list_taken = nullptr;
     uint2* d_list_not = nullptr;
@@ -548,9 +856,10 @@ void free_handle(rc_cohort* h) {
     if (h->device >= 0) {
         DeviceGuard g(h->device);
         (void)hipFree(h->d_offsets);
-        (void)hipFree(h->d_tab);
-        (void)hipFree(h->d_tools);
+        (void)hipFree(h->d_raw);
         (void)hipFree(h->d_cdf);
+        (void)hipFree(h->d_img);
+        (void)hipFree(h->d_span);
         (void)hipFree(h->d_wdesc);
         (void)hipFree(h->d_list_taken);
         (void)hipFree(h->d_list_not);
@@ -583,26 +892,32 @@ int validate_desc(const rc_cohort_desc* d) {
     return RC_OK;
 }
 
-// Pack cohorts into workgroups of nwave wavefronts (see the file comment).
-void build_plan(rc_cohort* h, std::vector<uint32_t>& wdesc) {
-    const uint32_t NW = h->nwave;
-    const std::vector<uint32_t>& off = h->offsets;
-    wdesc.clear();
-    h->bin_of_cohort.assign(h->C, 0);
-    uint32_t bin = 0, wave = 0, lane = 0;  // next free position
-    auto ensure_bin = [&](uint32_t b) {
-        if (wdesc.size() < (size_t)(b + 1) * NW * WD_WORDS) wdesc.resize((size_t)(b + 1) * NW * WD_WORDS, 0u);
+// Pack cohorts into bins of nw wavefronts (see the file comment): first every
+// cohort of at most 64 sessions, in order, then the larger ones.  Lanes of a
+// wavefront hold consecutive sessions, so two small cohorts share a
+// wavefront only when they are consecutive cohorts.
+void build_plan(const uint32_t* off, uint32_t C, uint32_t nw_per_bin, Plan& P) {
+    const uint32_t NW = nw_per_bin;
+    P.nwave = NW;
+    P.wdesc.clear();
+    P.bin_of_cohort.assign(C, 0);
+    int64_t bin = -1;        // open bin (-1: none)
+    uint32_t wave = 0, lane = 0;
+    uint32_t prev_c = 0;     // last cohort placed in the open wavefront (lane > 0)
+    auto open_bin = [&]() {
+        ++bin;
+        wave = 0;
+        lane = 0;
+        P.wdesc.resize((size_t)(bin + 1) * NW * WD_WORDS, 0u);
     };
-    ensure_bin(0);
-    for (uint32_t c = 0; c < h->C; ++c) {
+    auto place = [&](uint32_t c) {
         const uint32_t b = off[c], k = off[c + 1] - off[c];
         if (k > 64u) {
             const uint32_t nw = (k + 63u) / 64u;
             if (lane > 0u) { ++wave; lane = 0; }
-            if (wave + nw > NW) { ++bin; wave = 0; lane = 0; }
-            ensure_bin(bin);
+            if (bin < 0 || wave + nw > NW) open_bin();
             for (uint32_t i = 0; i < nw; ++i) {
-                uint32_t* d = &wdesc[((size_t)bin * NW + wave + i) * WD_WORDS];
+                uint32_t* d = &P.wdesc[((size_t)bin * NW + wave + i) * WD_WORDS];
                 d[WD_S0] = b + 64u * i;
                 d[WD_NACT] = (k - 64u * i) < 64u ? (k - 64u * i) : 64u;
                 d[WD_CFIRST] = c;
@@ -611,14 +926,13 @@ void build_plan(rc_cohort* h, std::vector<uint32_t>& wdesc) {
                 d[WD_KFIRST] = k;
                 d[WD_FLAGS] = WF_MULTI | (i << 8) | (nw << 16) | (wave << 24);
             }
-            h->bin_of_cohort[c] = bin;
+            P.bin_of_cohort[c] = (uint32_t)bin;
             wave += nw;
             lane = 0;
         } else {
-            if (lane + k > 64u) { ++wave; lane = 0; }
-            if (wave >= NW) { ++bin; wave = 0; lane = 0; }
-            ensure_bin(bin);
-            uint32_t* d = &wdesc[((size_t)bin * NW + wave) * WD_WORDS];
+            if (lane > 0u && (lane + k > 64u || c != prev_c + 1u)) { ++wave; lane = 0; }
+            if (bin < 0 || wave >= NW) open_bin();
+            uint32_t* d = &P.wdesc[((size_t)bin * NW + wave) * WD_WORDS];
             if (lane == 0u) {
                 d[WD_S0] = b;
                 d[WD_NACT] = 0;
@@ -630,23 +944,67 @@ void build_plan(rc_cohort* h, std::vector<uint32_t>& wdesc) {
             }
             d[WD_NACT] += k;
             d[WD_NCOH] += 1;
-            h->bin_of_cohort[c] = bin;
+            P.bin_of_cohort[c] = (uint32_t)bin;
             lane += k;
+            prev_c = c;
         }
+    };
+    for (uint32_t c = 0; c < C; ++c)
+        if (off[c + 1] - off[c] <= 64u) place(c);
+    P.n_bins_a = (uint32_t)(bin + 1);
+    wave = NW;  // the multi-wavefront class starts in a fresh bin
+    lane = 0;
+    for (uint32_t c = 0; c < C; ++c)
+        if (off[c + 1] - off[c] > 64u) place(c);
+    P.n_bins = (uint32_t)(bin + 1);
+
+    // class lookups for cohort ranges
+    P.first_a.assign(C + 1u, C);
+    P.first_b.assign(C + 1u, C);
+    for (int64_t c = (int64_t)C - 1; c >= 0; --c) {
+        const bool small = off[c + 1] - off[c] <= 64u;
+        P.first_a[c] = small ? (uint32_t)c : P.first_a[c + 1];
+        P.first_b[c] = small ? P.first_b[c + 1] : (uint32_t)c;
     }
-    h->n_bins = (uint32_t)(wdesc.size() / ((size_t)NW * WD_WORDS));
+    P.last_a.assign(C, -1);
+    P.last_b.assign(C, -1);
+    for (uint32_t c = 0; c < C; ++c) {
+        const bool small = off[c + 1] - off[c] <= 64u;
+        P.last_a[c] = small ? (int32_t)c : (c ? P.last_a[c - 1] : -1);
+        P.last_b[c] = small ? (c ? P.last_b[c - 1] : -1) : (int32_t)c;
+    }
+
     // mark workgroups that contain a multi-wavefront cohort; count idle lanes
     uint32_t idle = 0;
-    for (uint32_t bb = 0; bb < h->n_bins; ++bb) {
+    for (uint32_t bb = 0; bb < P.n_bins; ++bb) {
         bool any = false;
-        for (uint32_t w = 0; w < NW; ++w) any |= (wdesc[((size_t)bb * NW + w) * WD_WORDS + WD_FLAGS] & WF_MULTI) != 0u;
+        for (uint32_t w = 0; w < NW; ++w) any |= (P.wdesc[((size_t)bb * NW + w) * WD_WORDS + WD_FLAGS] & WF_MULTI) != 0u;
         for (uint32_t w = 0; w < NW; ++w) {
-            uint32_t* d = &wdesc[((size_t)bb * NW + w) * WD_WORDS];
+            uint32_t* d = &P.wdesc[((size_t)bb * NW + w) * WD_WORDS];
             if (any) d[WD_FLAGS] |= WF_WGMULTI;
             idle += 64u - d[WD_NACT];
         }
     }
-    h->idle_lanes = idle;
+    P.idle_lanes = idle;
+}
+
+// Bins covering the cohorts [cb, ce) (cb < ce): a range of sub-wavefront
+// bins and a range of multi-wavefront bins.
+void bins_of_range(const Plan& P, uint32_t cb, uint32_t ce, uint32_t& a_lo, uint32_t& a_n,
+                   uint32_t& b_lo, uint32_t& b_n) {
+    a_lo = a_n = b_lo = b_n = 0;
+    const uint32_t fa = P.first_a[cb];
+    if (fa < ce) {
+        const uint32_t la = (uint32_t)P.last_a[ce - 1];
+        a_lo = P.bin_of_cohort[fa];
+        a_n = P.bin_of_cohort[la] - a_lo + 1u;
+    }
+    const uint32_t fb = P.first_b[cb];
+    if (fb < ce) {
+        const uint32_t lb = (uint32_t)P.last_b[ce - 1];
+        b_lo = P.bin_of_cohort[fb];
+        b_n = P.bin_of_cohort[lb] - b_lo + 1u;
+    }
 }
 
 template <typename T>
@@ -672,7 +1030,7 @@ bool device_extent_ok(const void* p, size_t bytes, int dev) {
 
 int validate_buffers(const rc_cohort* h, const rc_buffers* b, uint32_t T) {
     if (!b) return RC_E_INVALID;
-    if (b->ld < h->N) return RC_E_INVALID;
+    if (b->ld < h->N || b->ld > RC_MAX_SESSIONS) return RC_E_INVALID;
     const uint64_t ld = b->ld;
     struct Ext { const void* p; uint64_t bytes; } ext[6] = {
         {b->state, 4ull * h->W * ld},
@@ -693,32 +1051,8 @@ int validate_buffers(const rc_cohort* h, const rc_buffers* b, uint32_t T) {
             if (a0 < b1 && b0 < a1) return RC_E_INVALID;
         }
     for (int i = 0; i < 6; ++i)
-        if (!device_extent_ok(ext[i].p, ext[i].bytes, h->device)) return RC_E_INVALID;
+        if (ext[i].bytes && !device_extent_ok(ext[i].p, ext[i].bytes, h->device)) return RC_E_INVALID;
     return RC_OK;
-}
-
-ChainArgs chain_args(const rc_cohort* h, const rc_buffers* b) {
-    ChainArgs a;
-    a.state = b->state;
-    a.outcome = b->outcome;
-    a.eff_sid = b->eff_sid;
-    a.eff_tool = b->eff_tool;
-    a.eff_payload = b->eff_payload;
-    a.n_taken = b->n_taken;
-    a.tab = h->d_tab;
-    a.tools = h->d_tools;
-    a.cdf = h->d_cdf;
-    a.offsets = h->d_offsets;
-    a.wdesc = h->d_wdesc;
-    a.ra = h->ra;
-    a.ld = b->ld;
-    a.n_words = h->W;
-    a.n_cohorts = h->C;
-    a.thr = h->thr;
-    a.lds_tools_off = h->lds_tools_off;
-    a.lds_cdf_off = h->lds_cdf_off;
-    a.lds_cnt_off = h->lds_cnt_off;
-    return a;
 }
 
 int launch_ok() {
@@ -727,16 +1061,32 @@ int launch_ok() {
 
 int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
                  uint32_t cb, uint32_t ce, hipStream_t stream) {
-    ChainArgs a = chain_args(h, b);
+    ChainArgs a;
+    a.state = b->state;
+    a.outcome = b->outcome;
+    a.eff_sid = b->eff_sid;
+    a.eff_tool = b->eff_tool;
+    a.eff_payload = b->eff_payload;
+    a.n_taken = b->n_taken;
+    a.img = h->d_img;
+    a.offsets = h->d_offsets;
+    a.wdesc = h->d_wdesc;
+    a.ra = h->ra;
+    a.ld = b->ld;
+    a.n_words = h->W;
+    a.n_cohorts = h->C;
+    a.thr = h->thr;
     a.step0 = step0;
     a.n_steps = T;
     a.cohort_begin = cb;
     a.cohort_end = ce;
-    a.bin_lo = h->bin_of_cohort[cb];
-    a.bin_hi = h->bin_of_cohort[ce - 1] + 1u;
-    const uint32_t bins = a.bin_hi - a.bin_lo;
-    const uint32_t grid = bins < h->max_grid ? bins : h->max_grid;
-    ChainFn fn = pick_chain(h->wmax, h->exact, h->nwave);
+    bins_of_range(h->plan, cb, ce, a.bins_a_lo, a.bins_a_n, a.bins_b_lo, a.bins_b_n);
+    a.img_words = h->img_words;
+    a.tools_off = h->tools_off;
+    a.cdf_off = h->cdf_off;
+    a.guide_off = h->guide_off;
+    const uint32_t grid = a.bins_a_n + a.bins_b_n;  // one workgroup per bin
+    ChainFn fn = pick_chain(h->wmax, h->exact, h->nwave, h->full);
     hipLaunchKernelGGL(fn, dim3(grid), dim3(h->nwave * 64), h->chain_lds_bytes, stream, a);
     if (launch_ok() != RC_OK) return RC_E_DEVICE;
     h->last_launches = 1;
@@ -752,10 +1102,9 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
         h->parity = 0;
         h->ctr_dirty = false;
     }
-    const uint32_t bin_lo = h->bin_of_cohort[cb];
-    const uint32_t bin_hi = h->bin_of_cohort[ce - 1] + 1u;
-    const uint32_t bins = bin_hi - bin_lo;
-    const uint32_t grid = bins < h->max_grid ? bins : h->max_grid;
+    uint32_t a_lo, a_n, b_lo, b_n;
+    bins_of_range(h->plan, cb, ce, a_lo, a_n, b_lo, b_n);
+    const uint32_t grid = a_n + b_n;
     const uint32_t n_range = h->offsets[ce] - h->offsets[cb];
     DecideFn dfn = pick_decide(h->nwave);
     BodyFn taken_fn = pick_body(h->wmax, h->exact, true);
@@ -778,8 +1127,10 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
         d.n_sessions = h->N;
         d.cohort_begin = cb;
         d.cohort_end = ce;
-        d.bin_lo = bin_lo;
-        d.bin_hi = bin_hi;
+        d.bins_a_lo = a_lo;
+        d.bins_a_n = a_n;
+        d.bins_b_lo = b_lo;
+        d.bins_b_n = b_n;
         d.parity = h->parity;
         hipLaunchKernelGGL(dfn, dim3(grid), dim3(h->nwave * 64), 0, stream, d);
         if (launch_ok() != RC_OK) return RC_E_DEVICE;
@@ -798,8 +1149,7 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
         ba.eff_sid = b->eff_sid;
         ba.eff_tool = b->eff_tool;
         ba.eff_payload = b->eff_payload;
-        ba.tab = h->d_tab;
-        ba.tools = h->d_tools;
+        ba.raw = h->d_raw;
         ba.cdf = h->d_cdf;
         ba.ra = h->ra;
         ba.ld = b->ld;
@@ -866,66 +1216,85 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     h->thr = desc->decide_thr;
     h->wmax = next_pow2_words(h->W);
     h->exact = (h->wmax == h->W);
-    h->ra.mode = desc->route_mode;
-    h->ra.n_routes = h->R;
-    h->ra.is_pow2 = (h->R & (h->R - 1u)) == 0u;
-    h->ra.pow2_mask = h->ra.is_pow2 ? h->R - 1u : 0u;
-    h->ra.cdf_n = (desc->route_mode == RC_ROUTE_CDF) ? h->R - 1u : 0u;
+    const uint32_t R = h->R;
+    // with a single route both route maps give route 0
+    h->ra.mode = (desc->route_mode == RC_ROUTE_CDF && R > 1u) ? RC_ROUTE_CDF : RC_ROUTE_MOD;
+    h->ra.n_routes = R;
+    h->ra.is_pow2 = (R & (R - 1u)) == 0u;
+    h->ra.pow2_mask = h->ra.is_pow2 ? R - 1u : 0u;
+    h->ra.cdf_n = (h->ra.mode == RC_ROUTE_CDF) ? R - 1u : 0u;
     h->ra.cdf_top = 0;
     while (h->ra.cdf_n && (h->ra.cdf_top << 1) <= h->ra.cdf_n && h->ra.cdf_top < (1u << 30))
         h->ra.cdf_top = h->ra.cdf_top ? h->ra.cdf_top << 1 : 1u;
 
-    // LDS image: (R+1) x 16 table words, rows 64 B with the four 16-byte
-    // blocks of row r rotated by r (bank spreading), row R all zero; then the
-    // packed tool pairs, the CDF thresholds and the popcount exchange.
-    const uint32_t R = h->R;
-    std::vector<uint32_t> tab((size_t)(R + 1) * 16u, 0u), tools(R, 0u);
-    for (uint32_t r = 0; r < R; ++r) {
-        for (uint32_t j = 0; j < 16; ++j) {
-            const uint32_t q = j >> 2, p = ((q + r) & 3u) * 4u + (j & 3u);
-            tab[(size_t)r * 16u + p] = desc->table[(size_t)r * 16u + j];
-        }
-        tools[r] = (desc->table[(size_t)r * 16u + 0] & 7u) | ((desc->table[(size_t)r * 16u + 1] & 7u) << 8);
+    // table image layout (see the file comment)
+    const size_t full_bytes = (size_t)(R + 1u) * h->wmax * 4u;
+    h->full = h->wmax <= 16u || full_bytes <= FULL_IMAGE_LIMIT;
+    const uint32_t row_words = h->full ? h->wmax : 16u;
+    const uint32_t tab_words = (R + 1u) * row_words;
+    h->tools_off = tab_words;
+    h->cdf_off = h->tools_off + (h->full ? ((R + 3u) & ~3u) : 0u);
+    h->guide_off = h->cdf_off + ((h->ra.cdf_n + 3u) & ~3u);
+    uint32_t guide_bits = 0, guide_n = 0;
+    if (h->ra.mode == RC_ROUTE_CDF) {
+        const uint32_t gmin = ceil_log2(R) < 1u ? 1u : ceil_log2(R);
+        guide_bits = gmin + 2u < 12u ? gmin + 2u : (gmin > 12u ? gmin : 12u);
+        while (guide_bits > gmin &&
+               ((size_t)h->guide_off + (((1u << guide_bits) + 1u + 3u) & ~3u)) * 4u + 256u > LDS_TWO_PER_CU)
+            --guide_bits;
+        guide_n = (1u << guide_bits) + 1u;
+        h->ra.guide_shift = 32u - guide_bits;
     }
-    const uint32_t tab_words = (R + 1u) * 16u;
-    h->lds_tools_off = tab_words;
-    h->lds_cdf_off = h->lds_tools_off + ((R + 3u) & ~3u);
-    h->lds_cnt_off = h->lds_cdf_off + ((h->ra.cdf_n + 3u) & ~3u);
-    const size_t lds_words = h->lds_cnt_off + 2u * 8u;
-    h->chain_lds_bytes = lds_words * 4u;
-    h->nwave = h->chain_lds_bytes > 40u * 1024u ? 8u : 4u;
+    h->img_words = h->guide_off + ((guide_n + 3u) & ~3u);
+    const size_t lds_image = (size_t)h->img_words * 4u;
+    h->nwave = (!h->full || lds_image > 40u * 1024u) ? 8u : 4u;
+    h->chain_lds_bytes = lds_image + 2u * (h->nwave + 4u) * 4u;
 
     h->offsets.assign(desc->cohort_offsets, desc->cohort_offsets + h->C + 1u);
-    std::vector<uint32_t> wdesc;
-    build_plan(h, wdesc);
+    build_plan(h->offsets.data(), h->C, h->nwave, h->plan);
 
     int rc = RC_OK;
     if (rc == RC_OK) rc = dev_upload(&h->d_offsets, h->offsets.data(), h->offsets.size() * 4u);
-    if (rc == RC_OK) rc = dev_upload(&h->d_tab, tab.data(), tab.size() * 4u);
-    if (rc == RC_OK) rc = dev_upload(&h->d_tools, tools.data(), tools.size() * 4u);
-    if (rc == RC_OK) {
-        if (h->ra.cdf_n) rc = dev_upload(&h->d_cdf, desc->route_cdf, (size_t)h->ra.cdf_n * 4u);
-        else rc = dev_upload(&h->d_cdf, nullptr, 0);
-    }
-    if (rc == RC_OK) rc = dev_upload(&h->d_wdesc, wdesc.data(), wdesc.size() * 4u);
+    if (rc == RC_OK) rc = dev_upload(&h->d_raw, desc->table, (size_t)R * 16u * 4u);
+    if (rc == RC_OK) rc = dev_upload(&h->d_cdf, desc->route_cdf, (size_t)h->ra.cdf_n * 4u);
+    if (rc == RC_OK && hipMalloc((void**)&h->d_img, (size_t)h->img_words * 4u) != hipSuccess) rc = RC_E_NOMEM;
+    if (rc == RC_OK && hipMalloc((void**)&h->d_span, 16) != hipSuccess) rc = RC_E_NOMEM;
+    if (rc == RC_OK && hipMemset(h->d_span, 0, 16) != hipSuccess) rc = RC_E_DEVICE;
+    if (rc == RC_OK) rc = dev_upload(&h->d_wdesc, h->plan.wdesc.data(), h->plan.wdesc.size() * 4u);
     if (rc == RC_OK && hipMalloc((void**)&h->d_list_taken, (size_t)h->N * sizeof(uint2)) != hipSuccess) rc = RC_E_NOMEM;
     if (rc == RC_OK && hipMalloc((void**)&h->d_list_not, (size_t)h->N * sizeof(uint2)) != hipSuccess) rc = RC_E_NOMEM;
     if (rc == RC_OK && hipMalloc((void**)&h->d_ctr, 4 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_NOMEM;
     if (rc == RC_OK && hipMemset(h->d_ctr, 0, 4 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_DEVICE;
     if (rc == RC_OK && hipHostMalloc((void**)&h->h_word, sizeof(uint32_t), hipHostMallocDefault) != hipSuccess) rc = RC_E_NOMEM;
-
     if (rc == RC_OK) {
-        ChainFn fn = pick_chain(h->wmax, h->exact, h->nwave);
-        if (hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)h->chain_lds_bytes) != hipSuccess) rc = RC_E_DEVICE;
-        int per_cu = 0;
-        if (rc == RC_OK && hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                               &per_cu, (const void*)fn, (int)(h->nwave * 64), h->chain_lds_bytes) != hipSuccess)
+        ImageArgs ia;
+        ia.raw = h->d_raw;
+        ia.cdf = h->d_cdf;
+        ia.img = h->d_img;
+        ia.max_span = h->d_span;
+        ia.n_routes = R;
+        ia.row_words = row_words;
+        ia.full = h->full ? 1u : 0u;
+        ia.tab_words = tab_words;
+        ia.tools_off = h->tools_off;
+        ia.cdf_off = h->cdf_off;
+        ia.cdf_n = h->ra.cdf_n;
+        ia.guide_off = h->guide_off;
+        ia.guide_n = guide_n;
+        ia.guide_shift = h->ra.guide_shift;
+        ia.total_words = h->img_words;
+        hipLaunchKernelGGL(rc_prep_kernel, dim3((h->img_words + 255u) / 256u), dim3(256), 0, 0, ia);
+        uint32_t span = 0;
+        if (launch_ok() != RC_OK || hipMemcpy(&span, h->d_span, 4, hipMemcpyDeviceToHost) != hipSuccess)
             rc = RC_E_DEVICE;
-        if (rc == RC_OK) {
-            if (per_cu < 1) per_cu = 1;
-            h->max_grid = (uint32_t)per_cu * (uint32_t)prop.multiProcessorCount;
-        }
+        h->ra.guide_top = 0;
+        while (span && (h->ra.guide_top << 1) <= span) h->ra.guide_top = h->ra.guide_top ? h->ra.guide_top << 1 : 1u;
+    }
+    if (rc == RC_OK) {
+        ChainFn fn = pick_chain(h->wmax, h->exact, h->nwave, h->full);
+        if (!fn) rc = RC_E_DEVICE;
+        if (rc == RC_OK && hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               (int)h->chain_lds_bytes) != hipSuccess) rc = RC_E_DEVICE;
     }
     if (rc != RC_OK) {
         (void)hipGetLastError();
@@ -973,9 +1342,38 @@ int rc_cohort_last_counts(const rc_cohort* h, uint32_t* launches, uint32_t* d2h_
 int rc_cohort_plan_info(const rc_cohort* h, uint32_t* n_workgroups, uint32_t* lanes_per_workgroup,
                         uint32_t* idle_lanes) {
     if (!h) return RC_E_INVALID;
-    if (n_workgroups) *n_workgroups = h->n_bins;
+    if (n_workgroups) *n_workgroups = h->plan.n_bins;
     if (lanes_per_workgroup) *lanes_per_workgroup = h->nwave * 64u;
-    if (idle_lanes) *idle_lanes = h->idle_lanes;
+    if (idle_lanes) *idle_lanes = h->plan.idle_lanes;
+    return RC_OK;
+}
+
+int rc_plan_lanes(const rc_cohort_desc* desc, uint32_t lanes_per_workgroup, uint32_t* lane_session,
+                  uint32_t* lane_cohort_out, uint32_t capacity, uint32_t* n_lanes) {
+    if (!n_lanes) return RC_E_INVALID;
+    const int v = validate_desc(desc);
+    if (v != RC_OK) return v;
+    if (lanes_per_workgroup != 256u && lanes_per_workgroup != 512u) return RC_E_INVALID;
+    Plan P;
+    build_plan(desc->cohort_offsets, desc->n_cohorts, lanes_per_workgroup / 64u, P);
+    const uint32_t total = P.n_bins * lanes_per_workgroup;
+    *n_lanes = total;
+    if (!lane_session || !lane_cohort_out) return RC_OK;
+    if (capacity < total) return RC_E_INVALID;
+    const uint32_t* off = desc->cohort_offsets;
+    for (uint32_t wv = 0; wv < P.n_bins * P.nwave; ++wv) {
+        const uint32_t* d = &P.wdesc[(size_t)wv * WD_WORDS];
+        for (uint32_t lane = 0; lane < 64u; ++lane) {
+            // the per-lane derivation of lane_cohort() in the kernels
+            const uint32_t s = d[WD_S0] + lane;
+            uint32_t c = d[WD_CFIRST];
+            for (uint32_t q = 1; q < d[WD_NCOH]; ++q)
+                if (off[d[WD_CFIRST] + q] <= s) c = d[WD_CFIRST] + q;
+            const bool act = lane < d[WD_NACT];
+            lane_session[wv * 64u + lane] = act ? s : 0xFFFFFFFFu;
+            lane_cohort_out[wv * 64u + lane] = act ? c : 0xFFFFFFFFu;
+        }
+    }
     return RC_OK;
 }
 

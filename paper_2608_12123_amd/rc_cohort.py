@@ -26,7 +26,7 @@ RC_MODE_RESIDENT, RC_MODE_HOST_ROUNDTRIP = 0, 1
 
 EXPORTED = [
     "rc_cohort_create", "rc_cohort_step", "rc_cohort_run_chain", "rc_cohort_destroy",
-    "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info",
+    "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info", "rc_plan_lanes",
 ]
 
 _P32 = ctypes.POINTER(ctypes.c_uint32)
@@ -95,6 +95,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rc_cohort_last_counts.restype = ctypes.c_int
     lib.rc_cohort_plan_info.argtypes = [ctypes.c_void_p, _P32, _P32, _P32]
     lib.rc_cohort_plan_info.restype = ctypes.c_int
+    lib.rc_plan_lanes.argtypes = [ctypes.POINTER(RcCohortDesc), ctypes.c_uint32, _P32, _P32,
+                                  ctypes.c_uint32, _P32]
+    lib.rc_plan_lanes.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -181,6 +184,24 @@ def rc_cohort_plan_info(h):
     return a.value, b.value, c.value
 
 
+def rc_plan_lanes(*, cohort_offsets, n_words=4, n_routes=1, lanes_per_workgroup=256):
+    """Host-only plan inspection: (lane_session, lane_cohort) uint32 arrays,
+    one entry per plan lane, 0xFFFFFFFF for idle lanes."""
+    lib = load_library()
+    off = _u32(cohort_offsets)
+    tab = np.zeros(n_routes * 16, dtype=np.uint32)
+    desc = RcCohortDesc(int(off[-1]), n_words, n_routes, off.size - 1, _ptr(off), _ptr(tab),
+                        RC_ROUTE_MOD, None, 32768)
+    n = ctypes.c_uint32()
+    _check(lib.rc_plan_lanes(ctypes.byref(desc), lanes_per_workgroup, None, None, 0,
+                             ctypes.byref(n)), "rc_plan_lanes")
+    ses = np.empty(n.value, dtype=np.uint32)
+    coh = np.empty(n.value, dtype=np.uint32)
+    _check(lib.rc_plan_lanes(ctypes.byref(desc), lanes_per_workgroup, _ptr(ses), _ptr(coh),
+                             n.value, ctypes.byref(n)), "rc_plan_lanes")
+    return ses, coh
+
+
 # ---------------------------------------------------------------------------
 # Device buffers (torch) for one handle
 # ---------------------------------------------------------------------------
@@ -223,7 +244,7 @@ class Cohort:
         T, ld, C = max_steps, self.ld, self.n_cohorts
         mk = lambda *shape: torch.full(shape, fill32, dtype=torch.int32, device=self.device)
         self.t = {"state": mk(n_words, ld), "outcome": mk(ld), "eff_sid": mk(T, ld),
-                  "eff_tool": mk(T, ld), "eff_payload": mk(T, 4, ld), "n_taken": mk(T, C)}
+                  "eff_tool": mk(T, ld), "eff_payload": mk(T, ld, 4), "n_taken": mk(T, C)}
         self.buffers = buffers_of(self.t, ld)
 
     @classmethod

@@ -208,7 +208,7 @@ def pin_taken_unit_table(oracle):
     res = single_run(oracle, words=[[0] * W], outcomes=[12345], table=[1] * 16, thr=65536,
                      n_routes=1)
     assert res["state"][:, 0].tolist() == [w + 1 for w in range(W)]
-    assert res["eff_payload"][0, :, 0].tolist() == [1, 2, 3, 4]
+    assert res["eff_payload"][0, 0, :].tolist() == [1, 2, 3, 4]
     assert res["n_taken"][0, 0] == 1
 
 
@@ -325,9 +325,9 @@ def pin_payload_post_update(oracle):
     """The emitted payload is the state after the update (taken, unit table:
     1, 2, 3, 4 from a zero state; not taken: rotl(0) + o = o)."""
     res = single_run(oracle, words=[[0] * 8], outcomes=[9], table=[1] * 16, thr=65536, n_routes=1)
-    assert res["eff_payload"][0, :, 0].tolist() == [1, 2, 3, 4]
+    assert res["eff_payload"][0, 0, :].tolist() == [1, 2, 3, 4]
     res = single_run(oracle, words=[[0] * 8], outcomes=[9], table=[1] * 16, thr=0, n_routes=1)
-    assert res["eff_payload"][0, :, 0].tolist() == [9, 9, 9, 9]
+    assert res["eff_payload"][0, 0, :].tolist() == [9, 9, 9, 9]
 
 
 def _decisions_by_pinned_rule(oracle, s0, o, step, thr):
@@ -373,7 +373,7 @@ def pin_chain_invariants(oracle):
             assert sorted(seg.tolist()) == list(range(offs[c], offs[c + 1]))  # each sid once
             assert 0 <= res["n_taken"][t, c] <= sizes[c]
         # padding slots never written
-        assert np.all(sid[t, N:] == 0xFFFFFFFF) and np.all(pay[t, :, N:] == 0xFFFFFFFF)
+        assert np.all(sid[t, N:] == 0xFFFFFFFF) and np.all(pay[t, N:, :] == 0xFFFFFFFF)
     # total effects = N * T
     assert int(np.sum(sid[:, :N] != 0xFFFFFFFF)) == N * T
     # O_{t+1} = fmix32(payload_t[0]) and the last payload is the final state
@@ -382,8 +382,8 @@ def pin_chain_invariants(oracle):
         pos[t] = np.empty(N, dtype=np.int64)
         pos[t][sid[t, :N]] = np.arange(N)
     for s in range(0, N, 7):
-        assert pay[T - 1, :, pos[T - 1][s]].tolist() == res["state"][:4, s].tolist()
-        assert res["outcome"][s] == pyref.fmix32(int(pay[T - 1, 0, pos[T - 1][s]]))
+        assert pay[T - 1, pos[T - 1][s], :].tolist() == res["state"][:4, s].tolist()
+        assert res["outcome"][s] == pyref.fmix32(int(pay[T - 1, pos[T - 1][s], 0]))
     # padding columns of state / outcome untouched
     assert np.all(res["state"][:, N:] == 0) and np.all(res["outcome"][N:] == 0)
 
@@ -480,7 +480,7 @@ def pin_brute_force_tiny(oracle, quick=False):
                     for t in range(2):
                         (sid, tool, pay), = p_e[t][i]
                         assert res["eff_sid"][t, i] == sid and res["eff_tool"][t, i] == tool
-                        assert tuple(res["eff_payload"][t, :, i].tolist()) == pay
+                        assert tuple(res["eff_payload"][t, i, :].tolist()) == pay
                         assert res["n_taken"][t, i] == p_c[t][i]
 
 
@@ -510,7 +510,7 @@ def pin_brute_force_cohorts(oracle):
                 sl = slice(offs[c], offs[c + 1])
                 assert res["eff_sid"][t, sl].tolist() == [x[0] for x in e]
                 assert res["eff_tool"][t, sl].tolist() == [x[1] for x in e]
-                assert res["eff_payload"][t, :, sl].T.tolist() == [list(x[2]) for x in e]
+                assert res["eff_payload"][t, sl, :].tolist() == [list(x[2]) for x in e]
                 assert res["n_taken"][t, c] == p_c[t][c]
 
 
