@@ -186,21 +186,30 @@ struct RouteArgs {
     uint32_t guide_top;   // largest step of the search inside a guide bucket
 };
 
-// Route key from the LDS thresholds and guide table (see the file comment).
+// Route kinds, fixed per kernel instantiation.
+enum : int { RK_POW2 = 0, RK_MOD = 1, RK_CDF = 2 };
+
+// Route key: o mod R, or (CDF) from the LDS thresholds and guide table (see
+// the file comment), with a branch-free search of fixed trip count.
+template <int RK>
 __device__ __forceinline__ uint32_t route_of(uint32_t o, const RouteArgs& ra,
                                              const uint32_t* cdf, const uint32_t* guide) {
-    if (ra.mode == RC_ROUTE_MOD)
-        return ra.is_pow2 ? (o & ra.pow2_mask) : (o % ra.n_routes);
-    const uint32_t bkt = o >> ra.guide_shift;
-    uint32_t pos = guide[bkt];
-    const uint32_t hi = guide[bkt + 1u];
-    for (uint32_t stp = ra.guide_top; stp != 0u; stp >>= 1) {
-        const uint32_t i = pos + stp;
-        const uint32_t j = i <= hi ? i : hi;
-        const uint32_t v = cdf[j == 0u ? 0u : j - 1u];
-        pos = (i <= hi && v <= o) ? i : pos;
+    if constexpr (RK == RK_POW2) {
+        return o & ra.pow2_mask;
+    } else if constexpr (RK == RK_MOD) {
+        return o % ra.n_routes;
+    } else {
+        const uint32_t bkt = o >> ra.guide_shift;
+        uint32_t pos = guide[bkt];
+        const uint32_t hi = guide[bkt + 1u];
+        for (uint32_t stp = ra.guide_top; stp != 0u; stp >>= 1) {
+            const uint32_t i = pos + stp;
+            const uint32_t j = i < hi ? i : hi;          // min(i, hi)
+            const uint32_t v = cdf[(j > 1u ? j : 1u) - 1u];  // always in range
+            pos = (i <= hi && v <= o) ? i : pos;
+        }
+        return pos;
     }
-    return pos;
 }
 
 // Route key by a plain fixed-trip binary search over all thresholds (used by
@@ -274,18 +283,34 @@ __device__ __forceinline__ LaneCohort lane_cohort(const uint32_t* __restrict__ w
 // wavefront.  Publication k goes to buffer k mod 2: its readers finish
 // before the barrier that follows publication k + 1, which precedes any
 // write of publication k + 2.
+__device__ __forceinline__ void publish_count(const LaneCohort& L, uint64_t bal, uint32_t lane,
+                                              uint32_t wv, uint32_t* cnt_lds, uint32_t cnt_stride,
+                                              uint32_t pub) {
+    if ((L.flags & WF_MULTI) && lane == 0u)
+        cnt_lds[(pub & 1u) * cnt_stride + wv] = (uint32_t)__popcll(bal);
+}
+
+// DEFER: the values are left in VGPRs and made uniform only when the slot is
+// computed, so the LDS latency overlaps other work; otherwise they move to
+// SGPRs at once (for kernels short of VGPRs).
+template <bool DEFER = false>
+__device__ __forceinline__ void barrier_read_counts(const LaneCohort& L, const uint32_t* cnt_lds,
+                                                    uint32_t cnt_stride, uint32_t& pub,
+                                                    uint32_t (&c4)[4]) {
+    __syncthreads();
+    if (L.flags & WF_MULTI) {
+        const uint32_t* buf = cnt_lds + (pub & 1u) * cnt_stride + (L.flags >> 24);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c4[i] = DEFER ? buf[i] : uni(buf[i]);
+    }
+    pub += 1u;
+}
+
 __device__ __forceinline__ void exchange_counts(const LaneCohort& L, uint64_t bal, uint32_t lane,
                                                 uint32_t wv, uint32_t* cnt_lds, uint32_t cnt_stride,
                                                 uint32_t& pub, uint32_t (&c4)[4]) {
-    uint32_t* buf = cnt_lds + (pub & 1u) * cnt_stride;
-    if ((L.flags & WF_MULTI) && lane == 0u) buf[wv] = (uint32_t)__popcll(bal);
-    __syncthreads();
-    if (L.flags & WF_MULTI) {
-        const uint32_t wf = L.flags >> 24;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) c4[i] = uni(buf[wf + i]);  // uniform: keep in SGPRs
-    }
-    pub += 1u;
+    publish_count(L, bal, lane, wv, cnt_lds, cnt_stride, pub);
+    barrier_read_counts(L, cnt_lds, cnt_stride, pub, c4);
 }
 
 // Stable-partition slot of this lane for a step with ballot `bal`; c4 holds
@@ -303,8 +328,9 @@ __device__ __forceinline__ uint32_t slot_of(const LaneCohort& L, bool dk, uint64
         uint32_t before = 0, total = 0;
 #pragma unroll
         for (uint32_t i = 0; i < 4; ++i) {
-            total += (i < nw) ? c4[i] : 0u;
-            before += (i < wi) ? c4[i] : 0u;
+            const uint32_t ci = uni(c4[i]);
+            total += (i < nw) ? ci : 0u;
+            before += (i < wi) ? ci : 0u;
         }
         n1 = total;
         rank_t = before + lane_rank(bal);
@@ -419,13 +445,15 @@ __device__ __forceinline__ void band0(uint32_t (&S)[WMAX], const uint32_t (&tv)[
                                       uint32_t (&M)[16], uint32_t sh, uint32_t oo, uint32_t W) {
     if constexpr (J < 16) {
         M[J] = mul_small<J + 1>(tv[J]);
-        if (J < WMAX && (EXACT || (uint32_t)J < W)) S[J < WMAX ? J : 0] = (rotr32(S[J < WMAX ? J : 0], sh) ^ M[J]) + oo;
+        if constexpr (J < WMAX)
+            if (EXACT || (uint32_t)J < W) S[J] = (rotr32(S[J], sh) ^ M[J]) + oo;
         band0<J + 1, EXACT, WMAX>(S, tv, M, sh, oo, W);
     }
 }
 
 // Table image, band B >= 1 (words 16 B .. 16 B + 15): the mask of w is the
-// mask of w - 16 plus table[r][w mod 16] << 4.
+// mask of w - 16 plus table[r][w mod 16] << 4; it is formed only after word
+// w - 16 is done, so one band of masks is live at a time.
 template <int B, bool EXACT, int WMAX>
 __device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[16],
                                      uint32_t (&M)[16], uint32_t sh, uint32_t oo, uint32_t W) {
@@ -437,7 +465,11 @@ __device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[1
     }
 }
 
-template <int WMAX, bool EXACT, int NWAVE, bool FULL>
+// One bin of the resident chain.  MULTI: the bin holds cohorts of more than
+// 64 sessions (every non-empty wavefront is part of one), so each step
+// exchanges popcounts behind a workgroup barrier; otherwise every cohort lies
+// inside one wavefront and no barrier is needed.
+template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool MULTI>
 struct Chain {
     static constexpr int MW = FULL ? WMAX : 16;
     static constexpr uint32_t CNT_STRIDE = NWAVE + 4;
@@ -453,15 +485,15 @@ struct Chain {
 
     // One chained step.  Full image: `mc` holds this step's masks and the
     // next step's row is prefetched into `mn`.  Table image: `mc` receives
-    // this step's table row.
+    // this step's table row.  The next step's decision is made (and, for
+    // MULTI, its popcount exchanged) even after the last step: the work is
+    // discarded, and every wavefront runs the same schedule.
     static __device__ __forceinline__ void step(const ChainArgs& a, const LaneCohort& L, Lane& st,
                                                 uint32_t t, uint32_t lane, uint32_t wv,
                                                 const uint32_t* lds, uint32_t* lds_cnt,
                                                 uint32_t (&mc)[MW], uint32_t (&mn)[MW]) {
         const uint32_t R = a.ra.n_routes;
         const uint32_t W = a.n_words;
-        const bool wgm = (L.flags & WF_WGMULTI) != 0u;
-        const bool has_next = t + 1u < a.n_steps;
 
         const uint32_t sh = opaque(st.dk ? 0u : ((31u - st.r) & 31u));
         const uint32_t oo = opaque(st.dk ? 0u : st.o);
@@ -484,17 +516,11 @@ struct Chain {
 
         // (a8) chain: next outcome; (a3, a4) the next step's route and decision
         const uint32_t o_n = dev_fmix32(st.S[0]);
-        uint32_t r_n = 0;
-        bool d_n = false;
-        uint64_t bal_n = 0;
-        uint32_t c4n[4] = {0u, 0u, 0u, 0u};
-        if (has_next) {
-            r_n = route_of(o_n, a.ra, lds + a.cdf_off, lds + a.guide_off);
-            d_n = L.active && ((dev_fmix32(st.S[0] ^ o_n ^ (st.step + 1u)) & 0xFFFFu) < a.thr);
-            bal_n = __ballot(d_n);
-            if (wgm) exchange_counts(L, bal_n, lane, wv, lds_cnt, CNT_STRIDE, st.pub, c4n);
-            if constexpr (FULL) load_row<MW>(lds, d_n ? r_n : R, mn);
-        }
+        const uint32_t r_n = route_of<RK>(o_n, a.ra, lds + a.cdf_off, lds + a.guide_off);
+        const bool d_n = L.active && ((dev_fmix32(st.S[0] ^ o_n ^ (st.step + 1u)) & 0xFFFFu) < a.thr);
+        const uint64_t bal_n = __ballot(d_n);
+        if constexpr (MULTI) publish_count(L, bal_n, lane, wv, lds_cnt, CNT_STRIDE, st.pub);
+        if constexpr (FULL) load_row<MW>(lds, d_n ? r_n : R, mn);
 
         // (a6) the remaining words
         if constexpr (FULL) {
@@ -502,8 +528,6 @@ struct Chain {
             for (int w = 4; w < WMAX; ++w)
                 if (EXACT || (uint32_t)w < W) st.S[w] = (rotr32(st.S[w], sh) ^ mc[w]) + oo;
         } else {
-            // band by band; a scheduling fence between bands keeps only one
-            // band's masks live
             band0<4, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
             __builtin_amdgcn_sched_barrier(0);
             if constexpr (WMAX > 16) {
@@ -517,11 +541,34 @@ struct Chain {
             }
         }
 
-        // (a5) compaction of this step; (a7) emit.  slot - b < k always holds;
-        // the test keeps a compaction defect from ever becoming a write outside
-        // the cohort's slots.
-        uint32_t n1;
-        const uint32_t slot = slot_of(L, st.dk, st.bal, st.c4, n1);
+        // the next step's counts: every wavefront has published by now
+        uint32_t c4n[4] = {0u, 0u, 0u, 0u};
+        if constexpr (MULTI) barrier_read_counts<FULL>(L, lds_cnt, CNT_STRIDE, st.pub, c4n);
+
+        // (a5) compaction of this step: stable partition, taken first
+        uint32_t n1, rank_t;
+        if constexpr (MULTI) {
+            const uint32_t wi = (L.flags >> 8) & 0xFFu;
+            const uint32_t nw = (L.flags >> 16) & 0xFFu;
+            uint32_t before = 0, total = 0;
+#pragma unroll
+            for (uint32_t i = 0; i < 4; ++i) {
+                const uint32_t ci = uni(st.c4[i]);
+                total += (i < nw) ? ci : 0u;
+                before += (i < wi) ? ci : 0u;
+            }
+            n1 = total;
+            rank_t = before + lane_rank(st.bal);
+        } else {
+            const uint64_t bs = st.bal & L.seg;
+            n1 = (uint32_t)__popcll(bs);
+            rank_t = lane_rank(bs);
+        }
+        const uint32_t in_c = L.s - L.b;
+        const uint32_t slot = L.b + (st.dk ? rank_t : n1 + (in_c - rank_t));
+
+        // (a7) emit.  slot - b < k always holds; the test keeps a compaction
+        // defect from ever becoming a write outside the cohort's slots.
         if (L.active && slot - L.b < L.k) {
             const size_t slice = (size_t)t * a.ld;
             st32(a.eff_sid + slice, slot << 2, L.s);
@@ -539,40 +586,41 @@ struct Chain {
         for (int i = 0; i < 4; ++i) st.c4[i] = c4n[i];
         st.step += 1u;
     }
-};
 
-// The table-image variant runs two 512-lane workgroups per CU, so it is held
-// to four wavefronts per SIMD (128 VGPRs).
-template <int WMAX, bool EXACT, int NWAVE, bool FULL>
-__global__ __launch_bounds__(NWAVE * 64, FULL ? 1 : 4) void rc_chain_kernel(ChainArgs a) {
-    using C = Chain<WMAX, EXACT, NWAVE, FULL>;
-    constexpr int MW = C::MW;
-    extern __shared__ uint4 lds4[];
-    uint32_t* lds = reinterpret_cast<uint32_t*>(lds4);
-    const uint32_t tid = threadIdx.x;
-    const uint32_t lane = tid & 63u;
-    const uint32_t wv = tid >> 6;
-    const uint32_t W = a.n_words;
-    const uint32_t R = a.ra.n_routes;
-    const uint32_t T = a.n_steps;
+    static __device__ __forceinline__ void run(const ChainArgs& a, uint32_t bin, uint4* lds4) {
+        uint32_t* lds = reinterpret_cast<uint32_t*>(lds4);
+        const uint32_t tid = threadIdx.x;
+        const uint32_t lane = tid & 63u;
+        const uint32_t wv = tid >> 6;
+        const uint32_t W = a.n_words;
+        const uint32_t R = a.ra.n_routes;
+        const uint32_t T = a.n_steps;
+        uint32_t* lds_cnt = lds + a.img_words;  // [2][NWAVE + 4]
 
-    // (a1) stage the table image once per workgroup
-    {
-        const uint4* src = reinterpret_cast<const uint4*>(a.img);
-        for (uint32_t i = tid; i < a.img_words / 4u; i += NWAVE * 64) lds4[i] = src[i];
-    }
-    __syncthreads();
-    uint32_t* lds_cnt = lds + a.img_words;  // [2][NWAVE + 4]
-    const uint32_t n_bins = a.bins_a_n + a.bins_b_n;
-    typename C::Lane st;
-    st.pub = 0;
+        // (a1) stage the table image (eight 16-byte loads per thread in flight)
+        {
+            const uint4* src = reinterpret_cast<const uint4*>(a.img);
+            const uint32_t n4 = a.img_words / 4u;
+            constexpr uint32_t WG = NWAVE * 64;
+            for (uint32_t j0 = tid; j0 < n4; j0 += 8u * WG) {
+                uint4 v[8];
+#pragma unroll
+                for (uint32_t k = 0; k < 8; ++k) {
+                    const uint32_t j = j0 + k * WG;
+                    v[k] = src[j < n4 ? j : n4 - 1u];
+                }
+#pragma unroll
+                for (uint32_t k = 0; k < 8; ++k)
+                    if (j0 + k * WG < n4) lds4[j0 + k * WG] = v[k];
+            }
+            __syncthreads();
+        }
 
-    for (uint32_t i = blockIdx.x; i < n_bins; i += gridDim.x) {
-        const uint32_t bin = i < a.bins_a_n ? a.bins_a_lo + i : a.bins_b_lo + (i - a.bins_a_n);
         const LaneCohort L = lane_cohort(a.wdesc + ((size_t)bin * NWAVE + wv) * WD_WORDS,
                                          a.offsets, lane, a.cohort_begin, a.cohort_end);
-        const bool wgm = (L.flags & WF_WGMULTI) != 0u;
         const uint32_t soff = L.s << 2;
+        Lane st;
+        st.pub = 0;
 
         // (a2) load the state words and the pending outcome
 #pragma unroll
@@ -588,19 +636,19 @@ __global__ __launch_bounds__(NWAVE * 64, FULL ? 1 : 4) void rc_chain_kernel(Chai
 
         // decision of the first step
         st.step = a.step0;
-        st.r = route_of(st.o, a.ra, lds + a.cdf_off, lds + a.guide_off);
+        st.r = route_of<RK>(st.o, a.ra, lds + a.cdf_off, lds + a.guide_off);
         st.dk = L.active && ((dev_fmix32(st.S[0] ^ st.o ^ st.step) & 0xFFFFu) < a.thr);
         st.bal = __ballot(st.dk);
 #pragma unroll
         for (int k = 0; k < 4; ++k) st.c4[k] = 0u;
-        if (wgm) exchange_counts(L, st.bal, lane, wv, lds_cnt, C::CNT_STRIDE, st.pub, st.c4);
+        if constexpr (MULTI) exchange_counts(L, st.bal, lane, wv, lds_cnt, CNT_STRIDE, st.pub, st.c4);
         uint32_t mA[MW], mB[MW];
         if constexpr (FULL) load_row<MW>(lds, st.dk ? st.r : R, mA);
 
         // T chained steps, unrolled by two so the prefetched row needs no copy
         for (uint32_t t = 0; t < T; t += 2u) {
-            C::step(a, L, st, t, lane, wv, lds, lds_cnt, mA, mB);
-            if (t + 1u < T) C::step(a, L, st, t + 1u, lane, wv, lds, lds_cnt, mB, mA);
+            step(a, L, st, t, lane, wv, lds, lds_cnt, mA, mB);
+            if (t + 1u < T) step(a, L, st, t + 1u, lane, wv, lds, lds_cnt, mB, mA);
         }
 
         // (a9) store the state and the next outcome (addresses recomputed
@@ -613,6 +661,18 @@ __global__ __launch_bounds__(NWAVE * 64, FULL ? 1 : 4) void rc_chain_kernel(Chai
             st32(a.outcome, soff, st.o);
         }
     }
+};
+
+// One workgroup per bin: blocks [0, bins_a_n) take the sub-wavefront bins,
+// the rest the multi-wavefront bins.  The table-image variant runs two
+// 512-lane workgroups per CU, so it is held to four wavefronts per SIMD.
+template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK>
+__global__ __launch_bounds__(NWAVE * 64, FULL ? 1 : 4) void rc_chain_kernel(ChainArgs a) {
+    extern __shared__ uint4 lds4[];
+    if (blockIdx.x < a.bins_a_n)
+        Chain<WMAX, EXACT, NWAVE, FULL, RK, false>::run(a, a.bins_a_lo + blockIdx.x, lds4);
+    else
+        Chain<WMAX, EXACT, NWAVE, FULL, RK, true>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
 }
 
 // ---------------------------------------------------------------------------
@@ -742,22 +802,29 @@ typedef void (*ChainFn)(ChainArgs);
 typedef void (*DecideFn)(DecideArgs);
 typedef void (*BodyFn)(BodyArgs);
 
-template <int WMAX, bool EXACT>
-ChainFn chain_fn(uint32_t nwave, bool full) {
+template <int WMAX, bool EXACT, int RK>
+ChainFn chain_fn(bool full) {
     if (!full) {
-        if constexpr (WMAX >= 32) return rc_chain_kernel<WMAX, EXACT, 8, false>;
+        if constexpr (WMAX >= 32) return rc_chain_kernel<WMAX, EXACT, 8, false, RK>;
         return nullptr;
     }
-    return nwave == 8 ? rc_chain_kernel<WMAX, EXACT, 8, true> : rc_chain_kernel<WMAX, EXACT, 4, true>;
+    return rc_chain_kernel<WMAX, EXACT, 4, true, RK>;
 }
 
-ChainFn pick_chain(uint32_t wmax, bool exact, uint32_t nwave, bool full) {
+template <int WMAX, bool EXACT>
+ChainFn chain_fn_rk(bool full, int rk) {
+    return rk == RK_POW2 ? chain_fn<WMAX, EXACT, RK_POW2>(full)
+         : rk == RK_MOD ? chain_fn<WMAX, EXACT, RK_MOD>(full)
+                        : chain_fn<WMAX, EXACT, RK_CDF>(full);
+}
+
+ChainFn pick_chain(uint32_t wmax, bool exact, bool full, int rk) {
     switch (wmax) {
-        case 4: return exact ? chain_fn<4, true>(nwave, full) : chain_fn<4, false>(nwave, full);
-        case 8: return exact ? chain_fn<8, true>(nwave, full) : chain_fn<8, false>(nwave, full);
-        case 16: return exact ? chain_fn<16, true>(nwave, full) : chain_fn<16, false>(nwave, full);
-        case 32: return exact ? chain_fn<32, true>(nwave, full) : chain_fn<32, false>(nwave, full);
-        default: return exact ? chain_fn<64, true>(nwave, full) : chain_fn<64, false>(nwave, full);
+        case 4: return exact ? chain_fn_rk<4, true>(full, rk) : chain_fn_rk<4, false>(full, rk);
+        case 8: return exact ? chain_fn_rk<8, true>(full, rk) : chain_fn_rk<8, false>(full, rk);
+        case 16: return exact ? chain_fn_rk<16, true>(full, rk) : chain_fn_rk<16, false>(full, rk);
+        case 32: return exact ? chain_fn_rk<32, true>(full, rk) : chain_fn_rk<32, false>(full, rk);
+        default: return exact ? chain_fn_rk<64, true>(full, rk) : chain_fn_rk<64, false>(full, rk);
     }
 }
 
@@ -829,6 +896,7 @@ struct rc_cohort {
     uint32_t wmax = 4;
     bool exact = true;
     bool full = true;
+    int route_kind = 0;  // RK_POW2 / RK_MOD / RK_CDF
     uint32_t nwave = 4;
     uint32_t img_words = 0, tools_off = 0, cdf_off = 0, guide_off = 0;
     size_t chain_lds_bytes = 0;
@@ -1086,7 +1154,7 @@ int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
     a.cdf_off = h->cdf_off;
     a.guide_off = h->guide_off;
     const uint32_t grid = a.bins_a_n + a.bins_b_n;  // one workgroup per bin
-    ChainFn fn = pick_chain(h->wmax, h->exact, h->nwave, h->full);
+    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind);
     hipLaunchKernelGGL(fn, dim3(grid), dim3(h->nwave * 64), h->chain_lds_bytes, stream, a);
     if (launch_ok() != RC_OK) return RC_E_DEVICE;
     h->last_launches = 1;
@@ -1223,6 +1291,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     h->ra.is_pow2 = (R & (R - 1u)) == 0u;
     h->ra.pow2_mask = h->ra.is_pow2 ? R - 1u : 0u;
     h->ra.cdf_n = (h->ra.mode == RC_ROUTE_CDF) ? R - 1u : 0u;
+    h->route_kind = h->ra.mode == RC_ROUTE_CDF ? RK_CDF : (h->ra.is_pow2 ? RK_POW2 : RK_MOD);
     h->ra.cdf_top = 0;
     while (h->ra.cdf_n && (h->ra.cdf_top << 1) <= h->ra.cdf_n && h->ra.cdf_top < (1u << 30))
         h->ra.cdf_top = h->ra.cdf_top ? h->ra.cdf_top << 1 : 1u;
@@ -1247,7 +1316,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     }
     h->img_words = h->guide_off + ((guide_n + 3u) & ~3u);
     const size_t lds_image = (size_t)h->img_words * 4u;
-    h->nwave = (!h->full || lds_image > 40u * 1024u) ? 8u : 4u;
+    h->nwave = h->full ? 4u : 8u;
     h->chain_lds_bytes = lds_image + 2u * (h->nwave + 4u) * 4u;
 
     h->offsets.assign(desc->cohort_offsets, desc->cohort_offsets + h->C + 1u);
@@ -1291,7 +1360,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
         while (span && (h->ra.guide_top << 1) <= span) h->ra.guide_top = h->ra.guide_top ? h->ra.guide_top << 1 : 1u;
     }
     if (rc == RC_OK) {
-        ChainFn fn = pick_chain(h->wmax, h->exact, h->nwave, h->full);
+        ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind);
         if (!fn) rc = RC_E_DEVICE;
         if (rc == RC_OK && hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                                (int)h->chain_lds_bytes) != hipSuccess) rc = RC_E_DEVICE;
