@@ -679,79 +679,73 @@ __global__ __launch_bounds__(NWAVE * 64, FULL ? 1 : 4) void rc_chain_kernel(Chai
 // Host round trip
 // ---------------------------------------------------------------------------
 
-// Part 1: decide and compact one step.  Writes n_taken, appends (sid, slot)
-// to the taken or not-taken list, and counts both populations in
-// ctr[parity][0..1] (ctr[parity][0] is the 4-byte word the host reads).
-// Block 0 clears the other parity's counters for the next step.
+// Part 1: decide and compact one step.  Writes n_taken and, for every
+// stepped session, perm[slot] = sid | d << 31 (the stable partition of each
+// cohort, in effect order), and adds the workgroup's taken count to
+// ctr[parity] (the 4-byte word the host reads), one global atomic per
+// workgroup.  Block 0 clears the other parity's counter for the next step.
 struct DecideArgs {
     const uint32_t* state;
     const uint32_t* outcome;
     uint32_t* n_taken;
-    uint2* list_taken;
-    uint2* list_not;
-    uint32_t* ctr;            // [2][2]
+    uint32_t* perm;           // [N]
+    uint32_t* ctr;            // [2]
     const uint32_t* offsets;
     const uint32_t* wdesc;
     uint32_t thr, step, t_index, n_cohorts, n_sessions;
     uint32_t cohort_begin, cohort_end;
-    uint32_t bins_a_lo, bins_a_n, bins_b_lo, bins_b_n, parity;
+    uint32_t bins_a_lo, bins_a_n, bins_b_lo, parity;
 };
 
 template <int NWAVE>
 __global__ __launch_bounds__(NWAVE * 64) void rc_decide_kernel(DecideArgs a) {
     __shared__ uint32_t cnt_lds[2 * (NWAVE + 4)];
+    __shared__ uint32_t wg_taken;
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
     const uint32_t wv = tid >> 6;
-    if (blockIdx.x == 0 && tid == 0) {
-        a.ctr[(a.parity ^ 1u) * 2u + 0u] = 0u;
-        a.ctr[(a.parity ^ 1u) * 2u + 1u] = 0u;
+    if (tid == 0u) {
+        wg_taken = 0u;
+        if (blockIdx.x == 0u) a.ctr[a.parity ^ 1u] = 0u;
     }
+    const uint32_t i = blockIdx.x;
+    const uint32_t bin = i < a.bins_a_n ? a.bins_a_lo + i : a.bins_b_lo + (i - a.bins_a_n);
+    const LaneCohort L = lane_cohort(a.wdesc + ((size_t)bin * NWAVE + wv) * WD_WORDS,
+                                     a.offsets, lane, a.cohort_begin, a.cohort_end);
+    uint32_t s0w = 0, o = 0;
+    if (L.active) {
+        s0w = ld32(a.state, L.s << 2);
+        o = ld32(a.outcome, L.s << 2);
+    }
+    const bool dk = L.active && ((dev_fmix32(s0w ^ o ^ a.step) & 0xFFFFu) < a.thr);
+    const uint64_t bal = __ballot(dk);
+    uint32_t c4[4] = {0u, 0u, 0u, 0u};
     uint32_t pub = 0;
-    const uint32_t n_bins = a.bins_a_n + a.bins_b_n;
-    for (uint32_t i = blockIdx.x; i < n_bins; i += gridDim.x) {
-        const uint32_t bin = i < a.bins_a_n ? a.bins_a_lo + i : a.bins_b_lo + (i - a.bins_a_n);
-        const LaneCohort L = lane_cohort(a.wdesc + ((size_t)bin * NWAVE + wv) * WD_WORDS,
-                                         a.offsets, lane, a.cohort_begin, a.cohort_end);
-        uint32_t s0w = 0, o = 0;
-        if (L.active) {
-            s0w = ld32(a.state, L.s << 2);
-            o = ld32(a.outcome, L.s << 2);
-        }
-        const bool dk = L.active && ((dev_fmix32(s0w ^ o ^ a.step) & 0xFFFFu) < a.thr);
-        const uint64_t bal = __ballot(dk);
-        uint32_t c4[4] = {0u, 0u, 0u, 0u};
-        if (L.flags & WF_WGMULTI) exchange_counts(L, bal, lane, wv, cnt_lds, NWAVE + 4, pub, c4);
-        uint32_t n1;
-        const uint32_t slot = slot_of(L, dk, bal, c4, n1);
-        if (L.active && L.s == L.b) a.n_taken[(size_t)a.t_index * a.n_cohorts + L.c] = n1;
-
-        const uint64_t bn = __ballot(L.active && !dk);
-        uint32_t base_t = 0, base_n = 0;
-        if (lane == 0u) {
-            if (bal) base_t = atomicAdd(&a.ctr[a.parity * 2u + 0u], (uint32_t)__popcll(bal));
-            if (bn) base_n = atomicAdd(&a.ctr[a.parity * 2u + 1u], (uint32_t)__popcll(bn));
-        }
-        base_t = uni(base_t);
-        base_n = uni(base_n);
-        const uint32_t at = dk ? base_t + lane_rank(bal) : base_n + lane_rank(bn);
-        if (L.active && at < a.n_sessions && slot - L.b < L.k)
-            (dk ? a.list_taken : a.list_not)[at] = make_uint2(L.s, slot);
-    }
+    __syncthreads();  // wg_taken is cleared
+    if (L.flags & WF_WGMULTI) exchange_counts(L, bal, lane, wv, cnt_lds, NWAVE + 4, pub, c4);
+    uint32_t n1;
+    const uint32_t slot = slot_of(L, dk, bal, c4, n1);
+    if (L.active && L.s == L.b) a.n_taken[(size_t)a.t_index * a.n_cohorts + L.c] = n1;
+    if (L.active && slot - L.b < L.k) a.perm[slot] = L.s | (dk ? 0x80000000u : 0u);
+    if (lane == 0u && bal) atomicAdd(&wg_taken, (uint32_t)__popcll(bal));
+    __syncthreads();
+    if (tid == 0u && wg_taken) atomicAdd(&a.ctr[a.parity], wg_taken);
 }
 
-// Part 2: the route body the host selected, over its compacted list.
+// Part 2: the route body the host selected.  Walks the slots [lo, hi) of
+// the stepped cohorts and handles the sessions of its own population, with
+// the slot the decide kernel assigned.
 struct BodyArgs {
     uint32_t* state;
     uint32_t* outcome;
     uint32_t* eff_sid;
     uint32_t* eff_tool;
     uint32_t* eff_payload;
-    const uint2* list;
+    const uint32_t* perm;
     const uint32_t* raw;   // [R][16]
     const uint32_t* cdf;
     RouteArgs ra;
-    uint32_t ld, n_words, count, t_index, n_sessions;
+    uint32_t ld, n_words, lo, hi, t_index, n_sessions;
 };
 
 template <int WMAX, bool EXACT, bool TAKEN>
@@ -762,12 +756,13 @@ __global__ __launch_bounds__(256) void rc_body_kernel(BodyArgs a) {
         for (uint32_t i = tid; i < a.ra.cdf_n; i += 256u) cdf_lds[i] = a.cdf[i];
         __syncthreads();
     }
-    const uint32_t i = blockIdx.x * 256u + tid;
-    if (i >= a.count) return;
+    const uint32_t slot = a.lo + blockIdx.x * 256u + tid;
+    if (slot >= a.hi) return;
+    const uint32_t e = a.perm[slot];
+    if ((e >> 31) != (TAKEN ? 1u : 0u)) return;
+    const uint32_t s = e & 0x7FFFFFFFu;
+    if (s >= a.n_sessions) return;  // never taken by a valid permutation
     const uint32_t W = a.n_words;
-    const uint2 e = a.list[i];
-    const uint32_t s = e.x, slot = e.y;
-    if (s >= a.n_sessions || slot >= a.n_sessions) return;  // never taken by valid lists
     const uint32_t soff = s << 2;
     const uint32_t o = ld32(a.outcome, soff);
     const uint32_t r = route_of_bsearch(o, a.ra, cdf_lds);
@@ -908,8 +903,7 @@ struct rc_cohort {
     uint32_t* d_img = nullptr;
     uint32_t* d_span = nullptr;
     uint32_t* d_wdesc = nullptr;
-    uint2* d_list_taken = nullptr;
-    uint2* d_list_not = nullptr;
+    uint32_t* d_perm = nullptr;  // host round trip: [N] slot -> sid | d << 31
     uint32_t* d_ctr = nullptr;
     uint32_t* h_word = nullptr;  // pinned
     uint32_t parity = 0;
@@ -929,8 +923,7 @@ void free_handle(rc_cohort* h) {
         (void)hipFree(h->d_img);
         (void)hipFree(h->d_span);
         (void)hipFree(h->d_wdesc);
-        (void)hipFree(h->d_list_taken);
-        (void)hipFree(h->d_list_not);
+        (void)hipFree(h->d_perm);
         (void)hipFree(h->d_ctr);
         if (h->h_word) (void)hipHostFree(h->h_word);
     }
@@ -1166,14 +1159,17 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
                        uint32_t cb, uint32_t ce, hipStream_t stream) {
     uint32_t launches = 0, copies = 0;
     if (h->ctr_dirty) {
-        if (hipMemsetAsync(h->d_ctr, 0, 4 * sizeof(uint32_t), stream) != hipSuccess) return RC_E_DEVICE;
+        // a previous call stopped inside a step: restart from cleared counters
+        if (hipMemsetAsync(h->d_ctr, 0, 2 * sizeof(uint32_t), stream) != hipSuccess) return RC_E_DEVICE;
         h->parity = 0;
         h->ctr_dirty = false;
     }
     uint32_t a_lo, a_n, b_lo, b_n;
     bins_of_range(h->plan, cb, ce, a_lo, a_n, b_lo, b_n);
     const uint32_t grid = a_n + b_n;
-    const uint32_t n_range = h->offsets[ce] - h->offsets[cb];
+    const uint32_t lo = h->offsets[cb], hi = h->offsets[ce];
+    const uint32_t n_range = hi - lo;
+    const uint32_t body_grid = (n_range + 255u) / 256u;
     DecideFn dfn = pick_decide(h->nwave);
     BodyFn taken_fn = pick_body(h->wmax, h->exact, true);
     BodyFn not_fn = pick_body(h->wmax, h->exact, false);
@@ -1183,8 +1179,7 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
         d.state = b->state;
         d.outcome = b->outcome;
         d.n_taken = b->n_taken;
-        d.list_taken = h->d_list_taken;
-        d.list_not = h->d_list_not;
+        d.perm = h->d_perm;
         d.ctr = h->d_ctr;
         d.offsets = h->d_offsets;
         d.wdesc = h->d_wdesc;
@@ -1198,13 +1193,12 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
         d.bins_a_lo = a_lo;
         d.bins_a_n = a_n;
         d.bins_b_lo = b_lo;
-        d.bins_b_n = b_n;
         d.parity = h->parity;
         hipLaunchKernelGGL(dfn, dim3(grid), dim3(h->nwave * 64), 0, stream, d);
         if (launch_ok() != RC_OK) return RC_E_DEVICE;
         ++launches;
         // the observation: 4 bytes to pinned host memory, then wait
-        if (hipMemcpyAsync(h->h_word, h->d_ctr + h->parity * 2u, sizeof(uint32_t),
+        if (hipMemcpyAsync(h->h_word, h->d_ctr + h->parity, sizeof(uint32_t),
                            hipMemcpyDeviceToHost, stream) != hipSuccess) return RC_E_DEVICE;
         ++copies;
         if (hipStreamSynchronize(stream) != hipSuccess) return RC_E_DEVICE;
@@ -1217,24 +1211,23 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
         ba.eff_sid = b->eff_sid;
         ba.eff_tool = b->eff_tool;
         ba.eff_payload = b->eff_payload;
+        ba.perm = h->d_perm;
         ba.raw = h->d_raw;
         ba.cdf = h->d_cdf;
         ba.ra = h->ra;
         ba.ld = b->ld;
         ba.n_words = h->W;
+        ba.lo = lo;
+        ba.hi = hi;
         ba.t_index = t;
         ba.n_sessions = h->N;
         if (n_taken_total > 0u) {
-            ba.list = h->d_list_taken;
-            ba.count = n_taken_total;
-            hipLaunchKernelGGL(taken_fn, dim3((n_taken_total + 255u) / 256u), dim3(256), 0, stream, ba);
+            hipLaunchKernelGGL(taken_fn, dim3(body_grid), dim3(256), 0, stream, ba);
             if (launch_ok() != RC_OK) return RC_E_DEVICE;
             ++launches;
         }
         if (n_taken_total < n_range) {
-            ba.list = h->d_list_not;
-            ba.count = n_range - n_taken_total;
-            hipLaunchKernelGGL(not_fn, dim3((ba.count + 255u) / 256u), dim3(256), 0, stream, ba);
+            hipLaunchKernelGGL(not_fn, dim3(body_grid), dim3(256), 0, stream, ba);
             if (launch_ok() != RC_OK) return RC_E_DEVICE;
             ++launches;
         }
@@ -1330,10 +1323,9 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     if (rc == RC_OK && hipMalloc((void**)&h->d_span, 16) != hipSuccess) rc = RC_E_NOMEM;
     if (rc == RC_OK && hipMemset(h->d_span, 0, 16) != hipSuccess) rc = RC_E_DEVICE;
     if (rc == RC_OK) rc = dev_upload(&h->d_wdesc, h->plan.wdesc.data(), h->plan.wdesc.size() * 4u);
-    if (rc == RC_OK && hipMalloc((void**)&h->d_list_taken, (size_t)h->N * sizeof(uint2)) != hipSuccess) rc = RC_E_NOMEM;
-    if (rc == RC_OK && hipMalloc((void**)&h->d_list_not, (size_t)h->N * sizeof(uint2)) != hipSuccess) rc = RC_E_NOMEM;
-    if (rc == RC_OK && hipMalloc((void**)&h->d_ctr, 4 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_NOMEM;
-    if (rc == RC_OK && hipMemset(h->d_ctr, 0, 4 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_DEVICE;
+    if (rc == RC_OK && hipMalloc((void**)&h->d_perm, (size_t)h->N * sizeof(uint32_t)) != hipSuccess) rc = RC_E_NOMEM;
+    if (rc == RC_OK && hipMalloc((void**)&h->d_ctr, 2 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_NOMEM;
+    if (rc == RC_OK && hipMemset(h->d_ctr, 0, 2 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_DEVICE;
     if (rc == RC_OK && hipHostMalloc((void**)&h->h_word, sizeof(uint32_t), hipHostMallocDefault) != hipSuccess) rc = RC_E_NOMEM;
     if (rc == RC_OK) {
         ImageArgs ia;
