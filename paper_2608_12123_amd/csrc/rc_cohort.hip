@@ -367,11 +367,17 @@ __global__ __launch_bounds__(256) void rc_prep_kernel(ImageArgs a) {
     const uint32_t R = a.n_routes;
     uint32_t v = 0;
     if (i < a.tab_words) {
-        const uint32_t WM = a.row_words, NB = WM / 4u;
-        const uint32_t r = i / WM, p = i % WM;
-        const uint32_t q = (p >> 2) ^ (r & (NB - 1u));
-        const uint32_t w = 4u * q + (p & 3u);
-        if (r < R) v = a.full ? a.raw[r * 16u + (w & 15u)] * (w + 1u) : a.raw[r * 16u + w];
+        if (a.full) {
+            // row r: W masks, then one zero block of padding
+            const uint32_t WM = a.row_words, RS = WM + 4u;
+            const uint32_t r = i / RS, w = i % RS;
+            if (r < R && w < WM) v = a.raw[r * 16u + (w & 15u)] * (w + 1u);
+        } else {
+            const uint32_t r = i / 16u, p = i % 16u;
+            const uint32_t q = (p >> 2) ^ (r & 3u);
+            const uint32_t w = 4u * q + (p & 3u);
+            if (r < R) v = a.raw[r * 16u + w];
+        }
     } else if (a.full && i >= a.tools_off && i < a.tools_off + R) {
         const uint32_t r = i - a.tools_off;
         v = (a.raw[r * 16u] & 7u) | ((a.raw[r * 16u + 1u] & 7u) << 8);
@@ -663,16 +669,288 @@ struct Chain {
     }
 };
 
+// Full-image chain, split by what each word depends on.  A session's route,
+// decision and next outcome at every step are functions of word 0 and the
+// outcome alone; every other word only follows the per-step (mask row,
+// rotation, addend) those choose.  Each chunk of up to TC steps runs as:
+//   chain:   word 0 alone through the chunk -- two hashes, the route and the
+//            decision per step -- recording (rotation | d << 5 | r << 6) and
+//            the addend of every step; no store;
+//   counts:  each wavefront publishes its taken count of every step of the
+//            chunk (cohorts spanning wavefronts), then one barrier;
+//   replay:  step by step, the words from the recorded control (one 16-byte
+//            LDS read and two VALU ops per four words), the stable-partition
+//            slot, and the effect stores.
+// SPLIT: two lanes per session.  Wavefronts [0, NWAVE) ("A") run the plan's
+// sessions: the chain, words [0, W/2), the slots and the effects.
+// Wavefronts [NWAVE, 2 NWAVE) ("B") mirror them lane for lane and replay
+// words [W/2, W) from the control the A lanes leave in LDS before the
+// chunk's barrier; a second barrier closes the chunk when another follows.
+// A lone wavefront issues VALU work at about half the rate a SIMD sustains
+// with several, so the second wavefront per session roughly halves the
+// replay.
+// Rows of the mask image are W + 4 words apart (one zero block of padding
+// shifts consecutive rows across the LDS banks), so block q of a row is an
+// immediate offset from the row's byte offset.
+template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT>
+struct ChainF {
+    static constexpr uint32_t CNT_STRIDE = NWAVE + 4;
+    static constexpr int WH = SPLIT ? WMAX / 2 : WMAX;  // words per lane
+    static constexpr int NBH = WH / 4;                   // 16-byte blocks per lane
+    static constexpr uint32_t RS = (WMAX + 4) * 4;       // row stride in bytes
+    static constexpr int TC = WMAX <= 32 ? 16 : 8;       // steps per chunk
+    static constexpr uint32_t WG = (SPLIT ? 2 : 1) * NWAVE * 64;
+    static constexpr int SB = WMAX <= 32 ? (SPLIT ? 5 : 10) : (SPLIT ? 3 : 6);
+
+    static __device__ __forceinline__ uint4 lds128(const uint32_t* lds, uint32_t byte_off) {
+        return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(lds) + byte_off);
+    }
+
+    static __device__ __forceinline__ void run(const ChainArgs& a, uint32_t bin, uint4* lds4) {
+        uint32_t* lds = reinterpret_cast<uint32_t*>(lds4);
+        const uint32_t tid = threadIdx.x;
+        const uint32_t lane = tid & 63u;
+        const uint32_t wv = uni(tid >> 6);
+        const bool role_b = SPLIT && wv >= (uint32_t)NWAVE;  // uniform per wavefront
+        const uint32_t wa = role_b ? wv - NWAVE : wv;         // the plan wavefront it serves
+        const uint32_t alane = wa * 64u + lane;                // lane index among the A lanes
+        const uint32_t wbase = role_b ? (uint32_t)WH : 0u;    // first word of this lane
+        const uint32_t W = a.n_words;
+        const uint32_t R = a.ra.n_routes;
+        const uint32_t T = a.n_steps;
+        uint32_t* lds_cnt = lds + a.img_words;          // [TC][NWAVE + 4]
+        uint32_t* lds_x = lds_cnt + TC * CNT_STRIDE;    // SPLIT: [TC][2][NWAVE * 64]
+        const uint32_t* lds_tools = lds + a.tools_off;
+
+        // (a1, a2) the lane's descriptor first (scalar loads), then the first
+        // batch of the table image, then the outcome and the state words.
+        // Vector-memory loads complete in order, so the image batch can be
+        // written to LDS while the state loads are still in flight.
+        const LaneCohort L = lane_cohort(a.wdesc + ((size_t)bin * NWAVE + wa) * WD_WORDS,
+                                         a.offsets, lane, a.cohort_begin, a.cohort_end);
+        const uint32_t soff = L.s << 2;
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4* src = reinterpret_cast<const u32x4*>(a.img);
+        u32x4* dst = reinterpret_cast<u32x4*>(lds4);
+        const uint32_t n4 = a.img_words / 4u;
+        u32x4 v[SB];
+#pragma unroll
+        for (int k = 0; k < SB; ++k) {
+            const uint32_t j = tid + (uint32_t)k * WG;
+            v[k] = src[j < n4 ? j : n4 - 1u];
+        }
+        // Unconditional loads (idle lanes read session 0 and never store), so
+        // that no branch splits the in-order load sequence.
+        uint32_t S[WH];
+        const uint32_t loff = L.active ? soff : 0u;
+        const uint32_t ldw = opaque_s(a.ld);
+        uint32_t o = ld32(a.outcome, loff);
+#pragma unroll
+        for (int w = 0; w < WH; ++w)
+            S[w] = (EXACT || wbase + (uint32_t)w < W) ? ld32(a.state + (size_t)(wbase + w) * ldw, loff) : 0u;
+        // Blocks past the image end repeat its last block (same value, same
+        // address), so the writes need no branch either.
+#pragma unroll
+        for (int k = 0; k < SB; ++k) {
+            const uint32_t j = tid + (uint32_t)k * WG;
+            dst[j < n4 ? j : n4 - 1u] = v[k];
+        }
+        for (uint32_t j = tid + (uint32_t)SB * WG; j < n4; j += WG) dst[j] = src[j];
+        __syncthreads();
+
+        // per-wavefront constants of the compaction
+        const uint32_t in_c = L.s - L.b;
+        bool f[4] = {false, false, false, false}, g[4] = {false, false, false, false};
+        if constexpr (MULTI) {
+            const uint32_t wi = (L.flags >> 8) & 0xFFu;
+            const uint32_t nw = (L.flags >> 16) & 0xFFu;
+#pragma unroll
+            for (uint32_t k = 0; k < 4; ++k) {
+                f[k] = k < wi;  // wavefronts of the cohort before this one
+                g[k] = k < nw;  // wavefronts of the cohort
+            }
+        }
+
+        uint32_t s0 = S[0];  // word 0 of the chain (A lanes)
+        uint32_t step = a.step0;
+        uint32_t* p_sid = a.eff_sid;
+        uint32_t* p_tool = a.eff_tool;
+        uint32_t* p_pay = a.eff_payload;
+        uint32_t* p_cnt = a.n_taken;
+
+        for (uint32_t t0 = 0; t0 < T; t0 += TC) {
+            const uint32_t n = (T - t0) < (uint32_t)TC ? (T - t0) : (uint32_t)TC;
+            uint32_t ctl[TC], add[TC];
+#pragma unroll
+            for (int i = 0; i < TC; ++i) {
+                ctl[i] = 0u;
+                add[i] = 0u;
+            }
+
+            if (!role_b) {
+                // chain: word 0 only
+                uint32_t r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
+                uint32_t m0 = lds[__umul24(r, RS) >> 2];  // taken mask of word 0, row r
+#pragma unroll
+                for (int i = 0; i < TC; ++i) {
+                    if ((uint32_t)i >= n) continue;
+                    const bool dk = L.active && ((dev_fmix32(s0 ^ o ^ step) & 0xFFFFu) < a.thr);
+                    const uint32_t sh = (31u - r) & 31u;
+                    const uint32_t oo = opaque(dk ? 0u : o);
+                    ctl[i] = (dk ? 32u : sh) | (r << 6);  // rotation 0 when taken
+                    add[i] = oo;
+                    s0 = (rotr32(s0, dk ? 0u : sh) ^ (dk ? m0 : 0u)) + oo;
+                    o = dev_fmix32(s0);
+                    r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
+                    m0 = lds[__umul24(r, RS) >> 2];
+                    step += 1u;
+                }
+                // counts of the chunk's steps: every lane writes the same
+                // (uniform) value to the same address, so no lane mask
+                if constexpr (MULTI) {
+#pragma unroll
+                    for (int i = 0; i < TC; ++i)
+                        lds_cnt[i * CNT_STRIDE + wa] = (uint32_t)__popcll(__ballot((ctl[i] >> 5) & 1u));
+                }
+                // the control for the B lanes
+                if constexpr (SPLIT) {
+#pragma unroll
+                    for (int i = 0; i < TC; ++i) {
+                        lds_x[(2 * i) * (NWAVE * 64) + alane] = ctl[i];
+                        lds_x[(2 * i + 1) * (NWAVE * 64) + alane] = add[i];
+                    }
+                }
+            }
+            if constexpr (MULTI || SPLIT) __syncthreads();
+            if (role_b) {
+#pragma unroll
+                for (int i = 0; i < TC; ++i) {
+                    ctl[i] = lds_x[(2 * i) * (NWAVE * 64) + alane];
+                    add[i] = lds_x[(2 * i + 1) * (NWAVE * 64) + alane];
+                }
+            }
+
+            // replay: this lane's words, and (A lanes) slots and effects, step
+            // by step.  The LDS reads of step i + 1 (mask blocks, counts, tool
+            // pair) are issued before step i is computed; past the chunk's
+            // last step they read the zero row (valid addresses, values
+            // unused).  The step count is re-read so that no per-step
+            // condition stays live across the phases.
+            const uint32_t nr = opaque_s(n);
+            const uint32_t* cq0 = lds_cnt + (L.flags >> 24);
+            const uint32_t qoff = wbase * 4u;  // byte offset of this lane's first block in a row
+            uint4 mc[NBH];
+            uint32_t cc[4], tpc;
+            {
+                const uint32_t c = ctl[0];
+                const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
+#pragma unroll
+                for (int q = 0; q < NBH; ++q) mc[q] = lds128(lds, rowoff + 16u * q);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[k] : 0u;
+                tpc = lds_tools[c >> 6];
+            }
+#pragma unroll
+            for (int i = 0; i < TC; ++i) {
+                uint4 mn[NBH];
+                uint32_t cn[4] = {0u, 0u, 0u, 0u}, tpn = 0u;
+                if (i + 1 < TC) {
+                    const uint32_t c = ctl[i + 1];
+                    const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
+#pragma unroll
+                    for (int q = 0; q < NBH; ++q) mn[q] = lds128(lds, rowoff + 16u * q);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) cn[k] = MULTI ? cq0[(i + 1) * CNT_STRIDE + k] : 0u;
+                    tpn = lds_tools[c >> 6];
+                }
+                if ((uint32_t)i < nr) {
+                    const uint32_t c = ctl[i];
+                    const bool dk = (c >> 5) & 1u;
+                    const uint32_t oo = add[i];
+#pragma unroll
+                    for (int q = 0; q < NBH; ++q) {
+                        if (!EXACT && wbase + (uint32_t)(4 * q) >= W) continue;
+                        S[4 * q] = (rotr32(S[4 * q], c) ^ mc[q].x) + oo;
+                        S[4 * q + 1] = (rotr32(S[4 * q + 1], c) ^ mc[q].y) + oo;
+                        S[4 * q + 2] = (rotr32(S[4 * q + 2], c) ^ mc[q].z) + oo;
+                        S[4 * q + 3] = (rotr32(S[4 * q + 3], c) ^ mc[q].w) + oo;
+                    }
+                    if (!role_b) {
+                        const uint32_t tool = (tpc >> (dk ? 8u : 0u)) & 7u;
+
+                        // (a5) stable partition, taken first
+                        const uint64_t bal = __ballot(dk);
+                        uint32_t n1, rank_t;
+                        if constexpr (MULTI) {
+                            n1 = (g[0] ? cc[0] : 0u) + (g[1] ? cc[1] : 0u) + (g[2] ? cc[2] : 0u) +
+                                 (g[3] ? cc[3] : 0u);
+                            rank_t = (f[0] ? cc[0] : 0u) + (f[1] ? cc[1] : 0u) + (f[2] ? cc[2] : 0u) +
+                                     lane_rank(bal);
+                        } else {
+                            const uint64_t bs = bal & L.seg;
+                            n1 = (uint32_t)__popcll(bs);
+                            rank_t = lane_rank(bs);
+                        }
+                        const uint32_t slot = L.b + (dk ? rank_t : n1 + (in_c - rank_t));
+
+                        // (a7) emit; slot - b < k always holds (the test keeps
+                        // a compaction defect from becoming a write outside
+                        // the cohort)
+                        if (L.active && slot - L.b < L.k) {
+                            st32(p_sid, slot << 2, L.s);
+                            st32(p_tool, slot << 2, tool);
+                            st128(p_pay, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
+                            if (in_c == 0u) st32(p_cnt, L.c << 2, n1);
+                        }
+                        p_sid += ldw;
+                        p_tool += ldw;
+                        p_pay += 4u * ldw;
+                        p_cnt += a.n_cohorts;
+                    }
+                }
+                if (i + 1 < TC) {
+#pragma unroll
+                    for (int q = 0; q < NBH; ++q) mc[q] = mn[q];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) cc[k] = cn[k];
+                    tpc = tpn;
+                }
+            }
+            // the counts and the control buffer are rewritten by the next
+            // chunk only after every wavefront has finished reading them
+            if constexpr (MULTI || SPLIT)
+                if (t0 + TC < T) __syncthreads();
+        }
+
+        // (a9) store the state and (A lanes) the next outcome
+        if (L.active) {
+#pragma unroll
+            for (int w = 0; w < WH; ++w)
+                if (EXACT || wbase + (uint32_t)w < W) st32(a.state + (size_t)(wbase + w) * ldw, soff, S[w]);
+            if (!role_b) st32(a.outcome, soff, o);
+        }
+    }
+};
+
 // One workgroup per bin: blocks [0, bins_a_n) take the sub-wavefront bins,
 // the rest the multi-wavefront bins.  The table-image variant runs two
 // 512-lane workgroups per CU, so it is held to four wavefronts per SIMD.
 template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK>
-__global__ __launch_bounds__(NWAVE * 64, FULL ? 1 : 4) void rc_chain_kernel(ChainArgs a) {
+__global__ __launch_bounds__((FULL && WMAX >= 32 ? 2 : 1) * NWAVE * 64, FULL ? 1 : 4)
+void rc_chain_kernel(ChainArgs a) {
     extern __shared__ uint4 lds4[];
-    if (blockIdx.x < a.bins_a_n)
-        Chain<WMAX, EXACT, NWAVE, FULL, RK, false>::run(a, a.bins_a_lo + blockIdx.x, lds4);
-    else
-        Chain<WMAX, EXACT, NWAVE, FULL, RK, true>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
+    if constexpr (FULL) {
+        constexpr bool SPLIT = WMAX >= 32;
+        if (blockIdx.x < a.bins_a_n)
+            ChainF<WMAX, EXACT, NWAVE, RK, false, SPLIT>::run(a, a.bins_a_lo + blockIdx.x, lds4);
+        else
+            ChainF<WMAX, EXACT, NWAVE, RK, true, SPLIT>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
+    } else {
+        if (blockIdx.x < a.bins_a_n)
+            Chain<WMAX, EXACT, NWAVE, FULL, RK, false>::run(a, a.bins_a_lo + blockIdx.x, lds4);
+        else
+            Chain<WMAX, EXACT, NWAVE, FULL, RK, true>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -895,6 +1173,7 @@ struct rc_cohort {
     uint32_t nwave = 4;
     uint32_t img_words = 0, tools_off = 0, cdf_off = 0, guide_off = 0;
     size_t chain_lds_bytes = 0;
+    uint32_t chain_threads = 256;  // threads of a chain workgroup
     std::vector<uint32_t> offsets;  // host copy [C+1]
     Plan plan;
     uint32_t* d_offsets = nullptr;
@@ -1148,7 +1427,7 @@ int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
     a.guide_off = h->guide_off;
     const uint32_t grid = a.bins_a_n + a.bins_b_n;  // one workgroup per bin
     ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind);
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(h->nwave * 64), h->chain_lds_bytes, stream, a);
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(h->chain_threads), h->chain_lds_bytes, stream, a);
     if (launch_ok() != RC_OK) return RC_E_DEVICE;
     h->last_launches = 1;
     h->last_d2h = 0;
@@ -1290,10 +1569,10 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
         h->ra.cdf_top = h->ra.cdf_top ? h->ra.cdf_top << 1 : 1u;
 
     // table image layout (see the file comment)
-    const size_t full_bytes = (size_t)(R + 1u) * h->wmax * 4u;
+    const size_t full_bytes = (size_t)(R + 1u) * (h->wmax + 4u) * 4u;
     h->full = h->wmax <= 16u || full_bytes <= FULL_IMAGE_LIMIT;
     const uint32_t row_words = h->full ? h->wmax : 16u;
-    const uint32_t tab_words = (R + 1u) * row_words;
+    const uint32_t tab_words = (R + 1u) * (h->full ? row_words + 4u : row_words);
     h->tools_off = tab_words;
     h->cdf_off = h->tools_off + (h->full ? ((R + 3u) & ~3u) : 0u);
     h->guide_off = h->cdf_off + ((h->ra.cdf_n + 3u) & ~3u);
@@ -1310,7 +1589,13 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     h->img_words = h->guide_off + ((guide_n + 3u) & ~3u);
     const size_t lds_image = (size_t)h->img_words * 4u;
     h->nwave = h->full ? 4u : 8u;
-    h->chain_lds_bytes = lds_image + 2u * (h->nwave + 4u) * 4u;
+    // image, then the count exchange ([16][nwave + 4] words; the table chain
+    // uses the first [2][nwave + 4]), then (full image, W >= 32: two lanes
+    // per session) the control handed to the second lanes, [16][2][nwave * 64]
+    const bool split = h->full && h->wmax >= 32u;
+    h->chain_threads = (split ? 2u : 1u) * h->nwave * 64u;
+    h->chain_lds_bytes = lds_image + 16u * (h->nwave + 4u) * 4u +
+                         (split ? 16u * 2u * h->nwave * 64u * 4u : 0u);
 
     h->offsets.assign(desc->cohort_offsets, desc->cohort_offsets + h->C + 1u);
     build_plan(h->offsets.data(), h->C, h->nwave, h->plan);
