@@ -922,11 +922,14 @@ struct ChainF {
                 if (t0 + TC < T) __syncthreads();
         }
 
-        // (a9) store the state and (A lanes) the next outcome
+        // (a9) store the state and (A lanes) the next outcome (the row
+        // addresses are recomputed from a fresh copy of ld rather than kept
+        // live across the chain)
         if (L.active) {
+            const uint32_t ld_st = opaque_s(a.ld);
 #pragma unroll
             for (int w = 0; w < WH; ++w)
-                if (EXACT || wbase + (uint32_t)w < W) st32(a.state + (size_t)(wbase + w) * ldw, soff, S[w]);
+                if (EXACT || wbase + (uint32_t)w < W) st32(a.state + (size_t)(wbase + w) * ld_st, soff, S[w]);
             if (!role_b) st32(a.outcome, soff, o);
         }
     }
