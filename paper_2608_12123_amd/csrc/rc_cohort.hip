@@ -68,6 +68,7 @@
 
 #include "rc_cohort.h"
 
+
 namespace {
 
 // ---------------------------------------------------------------------------
@@ -149,11 +150,22 @@ __device__ __forceinline__ uint32_t uni(uint32_t v) {
 __device__ __forceinline__ uint32_t ld32(const uint32_t* base, uint32_t byte_off) {
     return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(base) + byte_off);
 }
+// NT: nontemporal (streaming) store, for data the launch never reads again.
+// It raises the write bandwidth of fully written cache lines; lines that
+// several wavefronts fill piecewise are better left to the normal path.
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+template <bool NT = false>
 __device__ __forceinline__ void st32(uint32_t* base, uint32_t byte_off, uint32_t v) {
-    *reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(base) + byte_off) = v;
+    uint32_t* p = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(base) + byte_off);
+    if constexpr (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
 }
+template <bool NT = false>
 __device__ __forceinline__ void st128(uint32_t* base, uint32_t byte_off, uint4 v) {
-    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(base) + byte_off) = v;
+    u32x4v* p = reinterpret_cast<u32x4v*>(reinterpret_cast<char*>(base) + byte_off);
+    const u32x4v x = {v.x, v.y, v.z, v.w};
+    if constexpr (NT) __builtin_nontemporal_store(x, p);
+    else *p = x;
 }
 
 // Wavefront descriptor of the launch plan (8 x u32).
@@ -478,6 +490,10 @@ __device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[1
 template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool MULTI>
 struct Chain {
     static constexpr int MW = FULL ? WMAX : 16;
+    // Effect stores are nontemporal here: this path serves the large
+    // variable-cohort workloads, whose bins are mostly sub-wavefront cohorts
+    // that write whole lines per wavefront.
+    static constexpr bool NTE = true;
     static constexpr uint32_t CNT_STRIDE = NWAVE + 4;
 
     // Everything one lane carries from step to step.
@@ -577,10 +593,10 @@ struct Chain {
         // defect from ever becoming a write outside the cohort's slots.
         if (L.active && slot - L.b < L.k) {
             const size_t slice = (size_t)t * a.ld;
-            st32(a.eff_sid + slice, slot << 2, L.s);
-            st32(a.eff_tool + slice, slot << 2, tool);
-            st128(a.eff_payload + slice * 4u, slot << 4,
-                  make_uint4(st.S[0], st.S[1], st.S[2], st.S[3]));
+            st32<NTE>(a.eff_sid + slice, slot << 2, L.s);
+            st32<NTE>(a.eff_tool + slice, slot << 2, tool);
+            st128<NTE>(a.eff_payload + slice * 4u, slot << 4,
+                       make_uint4(st.S[0], st.S[1], st.S[2], st.S[3]));
             if (L.s == L.b) st32(a.n_taken + (size_t)t * a.n_cohorts, L.c << 2, n1);
         }
 
@@ -663,8 +679,8 @@ struct Chain {
             const uint32_t ldw = opaque_s(a.ld);
 #pragma unroll
             for (int w = 0; w < WMAX; ++w)
-                if (EXACT || (uint32_t)w < W) st32(a.state + (size_t)w * ldw, soff, st.S[w]);
-            st32(a.outcome, soff, st.o);
+                if (EXACT || (uint32_t)w < W) st32<true>(a.state + (size_t)w * ldw, soff, st.S[w]);
+            st32<true>(a.outcome, soff, st.o);
         }
     }
 };
@@ -694,6 +710,9 @@ struct Chain {
 // immediate offset from the row's byte offset.
 template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT>
 struct ChainF {
+    // Effect stores stay on the normal path: cohorts spanning wavefronts
+    // fill each line from several wavefronts.
+    static constexpr bool NTE = false;
     static constexpr uint32_t CNT_STRIDE = NWAVE + 4;
     static constexpr int WH = SPLIT ? WMAX / 2 : WMAX;  // words per lane
     static constexpr int NBH = WH / 4;                   // 16-byte blocks per lane
@@ -897,9 +916,9 @@ struct ChainF {
                         // a compaction defect from becoming a write outside
                         // the cohort)
                         if (L.active && slot - L.b < L.k) {
-                            st32(p_sid, slot << 2, L.s);
-                            st32(p_tool, slot << 2, tool);
-                            st128(p_pay, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
+                            st32<NTE>(p_sid, slot << 2, L.s);
+                            st32<NTE>(p_tool, slot << 2, tool);
+                            st128<NTE>(p_pay, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
                             if (in_c == 0u) st32(p_cnt, L.c << 2, n1);
                         }
                         p_sid += ldw;
@@ -929,8 +948,8 @@ struct ChainF {
             const uint32_t ld_st = opaque_s(a.ld);
 #pragma unroll
             for (int w = 0; w < WH; ++w)
-                if (EXACT || wbase + (uint32_t)w < W) st32(a.state + (size_t)(wbase + w) * ld_st, soff, S[w]);
-            if (!role_b) st32(a.outcome, soff, o);
+                if (EXACT || wbase + (uint32_t)w < W) st32<true>(a.state + (size_t)(wbase + w) * ld_st, soff, S[w]);
+            if (!role_b) st32<true>(a.outcome, soff, o);
         }
     }
 };
