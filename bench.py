@@ -220,6 +220,34 @@ def mechanism_row(rc, wk, key, budget_s=1.0):
     }
 
 
+def hbm_measured(n_bytes=512 << 20, reps=10):
+    """Context for the roofline: what plain streaming kernels (torch's device
+    copy and fill) reach on this GPU, timed with HIP events over `reps`
+    dispatches of `n_bytes` each.  Copy counts bytes read plus bytes written."""
+    import torch
+    n = n_bytes // 4
+    src = torch.ones(n, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    out = {}
+    for name, fn, moved in (("copy", lambda: dst.copy_(src), 2 * n_bytes),
+                            ("fill", lambda: dst.fill_(7), n_bytes)):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name + "_GBps"] = round(moved * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    out["bytes_per_dispatch"] = n_bytes
+    out["note"] = ("torch device copy (read + write) and fill (write only) of 512 MiB; "
+                   "context for the 8 TB/s spec peak, not the roofline peak")
+    del src, dst
+    return out
+
+
 def cpu_baseline(inp, T, min_seconds):
     """The oracle (plain single-threaded C) on the same workload, repeated
     until at least ``min_seconds`` of CPU work; also returns its outputs of
@@ -366,6 +394,7 @@ def main():
         }
         if cpu is not None:
             out["cpu_baseline"] = cpu
+        out["hbm_measured"] = hbm_measured()
         if not args.no_mechanisms:
             out["mechanisms"] = {k: mechanism_row(rc, wk, k) for k in wk.WORKLOAD_ORDER}
     rc.rc_cohort_destroy(h)
