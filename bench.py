@@ -150,6 +150,57 @@ def time_resident_synced(rc, h, sets, inp, T, steps, stream, ranges):
     return time.perf_counter() - t0
 
 
+def decisions_from_effects(eff_sid, n_taken, offsets, ld):
+    """The decision bitmap ([T][ceil(ld/32)] uint32) a chain made, read back
+    from its effect log: within each cohort's slots the first n_taken[t][c]
+    hold the taken sessions (the stable partition puts them first)."""
+    T = eff_sid.shape[0]
+    off = np.asarray(offsets, dtype=np.int64)
+    sizes = np.diff(off)
+    slot_rank = np.arange(off[-1]) - np.repeat(off[:-1], sizes)
+    dec = np.zeros((T, ld), dtype=bool)
+    for t in range(T):
+        taken_slot = slot_rank < np.repeat(n_taken[t].astype(np.int64), sizes)
+        dec[t, eff_sid[t, :off[-1]][taken_slot].astype(np.int64)] = True
+    words = np.zeros((T, (ld + 31) // 32), dtype=np.uint64)
+    for b in range(32):
+        col = dec[:, b::32]
+        words[:, :col.shape[1]] |= col.astype(np.uint64) << np.uint64(b)
+    return words.astype(np.uint32)
+
+
+def floor_bits(rc, h, inp, T, stream):
+    """Device decision bitmap for the no-decision floor: the decisions one
+    resident chain over every cohort makes on fresh inputs."""
+    import torch
+    one = Sets(rc, inp, T, 1)
+    rc.rc_cohort_run_chain(h, one[0], 0, T, rc.RC_MODE_RESIDENT, 0, inp.n_cohorts, stream)
+    torch.cuda.synchronize()
+    t = one.tensors(0)
+    bits = decisions_from_effects(t["eff_sid"].cpu().numpy().view(np.uint32),
+                                  t["n_taken"].cpu().numpy().view(np.uint32),
+                                  inp.cohort_offsets, inp.ld)
+    return torch.from_numpy(bits.view(np.int32)).cuda()
+
+
+def time_floor(rc, h, sets, bits, inp, T, steps, warmup, stream, ranges=None):
+    """Pipelined no-decision-floor launches (same protocol as the resident
+    chain).  Returns the wall seconds of the timed loop."""
+    import torch
+    rng = ranges or [(0, inp.n_cohorts)]
+    ptr = bits.data_ptr()
+    for i in range(warmup):
+        cb, ce = rng[i % len(rng)]
+        rc.rc_cohort_run_floor(h, sets[i], ptr, T, cb, ce, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        cb, ce = rng[i % len(rng)]
+        rc.rc_cohort_run_floor(h, sets[i], ptr, T, cb, ce, stream)
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
 def time_hrt(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
     import torch
     C = inp.n_cohorts
@@ -194,6 +245,8 @@ def mechanism_row(rc, wk, key, budget_s=1.0):
         res_counts = rc.rc_cohort_last_counts(h)
         n_sync = max(10, n // 4)
         wall_s = time_resident_synced(rc, h, sets, inp, T, n_sync, stream, ranges)
+        bits = floor_bits(rc, h, inp, T, stream)
+        wall_f = time_floor(rc, h, sets, bits, inp, T, n, 5, stream, ranges)
         w1 = time_hrt(rc, h, sets, inp, T, 3, 1, stream, ranges)
         n_h = int(max(5, min(n, budget_s / 2 / max(w1 / 3, 1e-7))))
         wall_h = time_hrt(rc, h, sets, inp, T, n_h, 0, stream, ranges)
@@ -203,6 +256,7 @@ def mechanism_row(rc, wk, key, budget_s=1.0):
     finally:
         rc.rc_cohort_destroy(h)
     us_r, us_s, us_h = wall_r / n * 1e6, wall_s / n_sync * 1e6, wall_h / n_h * 1e6
+    us_f = wall_f / n * 1e6
     return {
         "workload": wl.title, "T": T, "transitions_per_invocation": per_inv,
         "resident_us_per_invocation": round(us_r, 3),
@@ -212,11 +266,13 @@ def mechanism_row(rc, wk, key, budget_s=1.0):
         "host_rt_us_per_chained_step": round(us_h / T, 4),
         "host_over_resident": round(us_h / us_r, 3),
         "host_over_resident_synced": round(us_h / us_s, 3),
+        "floor_us_per_invocation": round(us_f, 3),
+        "resident_over_floor": round(us_r / us_f, 3),
         "resident_transitions_per_s": round(per_inv / (us_r * 1e-6), 1),
         "host_rt_transitions_per_s": round(per_inv / (us_h * 1e-6), 1),
         "launches_per_invocation": {"resident": res_counts[0], "host_rt": hrt_counts[0]},
         "d2h_copies_per_invocation": {"resident": res_counts[1], "host_rt": hrt_counts[1]},
-        "invocations_timed": {"resident": n, "resident_synced": n_sync, "host_rt": n_h},
+        "invocations_timed": {"resident": n, "resident_synced": n_sync, "host_rt": n_h, "floor": n},
     }
 
 
@@ -391,6 +447,15 @@ def main():
             "us_per_invocation": round(us_h, 3), "us_per_chained_step": round(us_h / T, 4),
             "host_over_resident": round(us_h / (ms_per_step * 1e3), 3),
             "launches_per_invocation": cnt[0], "d2h_copies_per_invocation": cnt[1], "steps": hs,
+        }
+        bits = floor_bits(rc, h, inp, T, stream)
+        wall_f = time_floor(rc, h, sets, bits, inp, T, args.steps, args.warmup, stream)
+        us_f = wall_f / args.steps * 1e6
+        out["floor"] = {
+            "us_per_invocation": round(us_f, 3), "us_per_chained_step": round(us_f / T, 4),
+            "resident_over_floor": round(ms_per_step * 1e3 / us_f, 3),
+            "note": "no-decision floor: the resident chain replaying a recorded decision "
+                    "bitmap with no predicate (a structural floor, not an online policy)",
         }
         if cpu is not None:
             out["cpu_baseline"] = cpu

@@ -163,6 +163,31 @@ int rc_cohort_run_chain(rc_cohort *h, const rc_buffers *b, uint32_t step0,
                         uint32_t n_steps, int mode, uint32_t cohort_begin,
                         uint32_t cohort_end, void *hip_stream);
 
+/*
+ * The no-decision floor (Section 7 "Matched mechanisms": the recorded route
+ * sequence replayed with no predicate and no selection; a structural floor
+ * for the two mechanisms above, not an admissible online policy).  It is the
+ * resident chain of n_steps steps with one change: the decision of session s
+ * at chained step t is read from `decisions` instead of computed by the
+ * predicate, so no step number is involved.  Routes, updates, the
+ * stable-partition compaction, effects, taken counts and the chained
+ * outcome are computed exactly as in rc_cohort_run_chain; given the
+ * decisions that rc_cohort_run_chain(step0, ...) makes on the same inputs,
+ * the outputs are bit-identical to it.
+ *   decisions  caller-owned DEVICE memory of the handle's device, read only:
+ *              [n_steps][dwords] uint32 with dwords = ceil(b->ld / 32); bit
+ *              (s mod 32) of word [t][s / 32] is session s's decision at
+ *              step t (1 = taken).  Bits of sessions outside the stepped
+ *              cohorts are ignored.  It must not overlap any buffer of `b`.
+ * One kernel launch, enqueued on `hip_stream`; returns without waiting.
+ * n_steps == 0 or an empty cohort range is a no-op.  Errors: those of
+ * rc_cohort_run_chain, and RC_E_INVALID when `decisions` is NULL, overlaps a
+ * buffer or is not device memory large enough for its extent.
+ */
+int rc_cohort_run_floor(rc_cohort *h, const rc_buffers *b, const uint32_t *decisions,
+                        uint32_t n_steps, uint32_t cohort_begin, uint32_t cohort_end,
+                        void *hip_stream);
+
 /* Release the handle's device and host resources.  Waits for nothing: the
  * caller synchronizes its streams first.  rc_cohort_destroy(NULL) is RC_OK. */
 int rc_cohort_destroy(rc_cohort *h);
@@ -172,9 +197,10 @@ const char *rc_status_string(int status);
 
 /*
  * Kernel launches and device-to-host copies enqueued by the last successful
- * rc_cohort_run_chain / rc_cohort_step on this handle (resident: 1 and 0;
- * host round trip: at least T + 1 launches and exactly T copies).  Either
- * output pointer may be NULL.  RC_E_INVALID when h is NULL.
+ * rc_cohort_run_chain / rc_cohort_step / rc_cohort_run_floor on this handle
+ * (resident and floor: 1 and 0; host round trip: at least T + 1 launches
+ * and exactly T copies).  Either output pointer may be NULL.  RC_E_INVALID
+ * when h is NULL.
  */
 int rc_cohort_last_counts(const rc_cohort *h, uint32_t *launches, uint32_t *d2h_copies);
 

@@ -79,8 +79,12 @@ class Oracle:
         lib.rc_oracle_update_word.restype = u32
         lib.rc_oracle_run_chain.argtypes = (
             [u32, u32, u32, u32, p32, p32, u32, p32, u32]
-            + [p32] * 6 + [u32, u32, u32, u32, u32])
+            + [p32] * 6 + [u32, u32, u32, u32, u32, p32])
         lib.rc_oracle_run_chain.restype = ctypes.c_int
+        lib.rc_oracle_run_floor.argtypes = (
+            [u32, u32, u32, u32, p32, p32, u32, p32, p32]
+            + [p32] * 6 + [u32, u32, u32, u32])
+        lib.rc_oracle_run_floor.restype = ctypes.c_int
         lib.rc_oracle_count_taken_all_outcomes.argtypes = [u32, u32, u32]
         lib.rc_oracle_count_taken_all_outcomes.restype = ctypes.c_uint64
         lib.rc_oracle_route_histogram.argtypes = [
@@ -124,13 +128,18 @@ class Oracle:
     def run_chain(self, *, n_words, n_routes, cohort_offsets, table, route_mode,
                   route_cdf, decide_thr, state, outcome, n_steps, step0=0,
                   cohort_begin=0, cohort_end=None, eff_sid=None, eff_tool=None,
-                  eff_payload=None, n_taken=None):
+                  eff_payload=None, n_taken=None, decisions=None, record=False):
         """Run ``n_steps`` chained steps in place.
 
         ``state`` is ``[W][ld]`` uint32 and ``outcome`` ``[ld]`` uint32; both
         are updated in place.  Effect arrays (``[T][ld]``, ``[T][ld]``,
         ``[T][ld][4]``) and ``n_taken`` (``[T][C]``) are allocated filled with
         ``0xFFFFFFFF`` when not given.  Returns a dict of the output arrays.
+
+        ``decisions``: a ``[T][ceil(ld/32)]`` uint32 bitmap; when given, the
+        no-decision floor runs instead (decisions read from it, no
+        predicate).  ``record``: also return the decisions made, as such a
+        bitmap (zero for sessions not stepped), under ``"decisions"``.
         """
         offsets = _u32(cohort_offsets)
         n_cohorts = offsets.size - 1
@@ -153,17 +162,35 @@ class Oracle:
             eff_payload = np.full((T, ld, 4), fill, dtype=np.uint32)
         if n_taken is None:
             n_taken = np.full((T, n_cohorts), fill, dtype=np.uint32)
-        rc = self.lib.rc_oracle_run_chain(
-            n_sessions, n_words, n_routes, n_cohorts, _p32(offsets), _p32(table),
-            route_mode, _p32(cdf), decide_thr, _p32(state), _p32(outcome),
-            _p32(eff_sid), _p32(eff_tool), _p32(eff_payload), _p32(n_taken),
-            ld, step0 & 0xFFFFFFFF, T, cohort_begin, cohort_end)
-        if rc != 0:
-            raise ValueError("rc_oracle_run_chain returned %d" % rc)
-        return {"state": state, "outcome": outcome, "eff_sid": eff_sid,
-                "eff_tool": eff_tool, "eff_payload": eff_payload, "n_taken": n_taken}
+        dwords = (ld + 31) // 32
+        if decisions is not None:
+            bits = _u32(decisions)
+            assert bits.shape == (T, dwords), "decisions must be [T][ceil(ld/32)]"
+            rc = self.lib.rc_oracle_run_floor(
+                n_sessions, n_words, n_routes, n_cohorts, _p32(offsets), _p32(table),
+                route_mode, _p32(cdf), _p32(bits), _p32(state), _p32(outcome),
+                _p32(eff_sid), _p32(eff_tool), _p32(eff_payload), _p32(n_taken),
+                ld, T, cohort_begin, cohort_end)
+            if rc != 0:
+                raise ValueError("rc_oracle_run_floor returned %d" % rc)
+            rec = None
+        else:
+            rec = np.zeros((T, dwords), dtype=np.uint32) if record else None
+            rc = self.lib.rc_oracle_run_chain(
+                n_sessions, n_words, n_routes, n_cohorts, _p32(offsets), _p32(table),
+                route_mode, _p32(cdf), decide_thr, _p32(state), _p32(outcome),
+                _p32(eff_sid), _p32(eff_tool), _p32(eff_payload), _p32(n_taken),
+                ld, step0 & 0xFFFFFFFF, T, cohort_begin, cohort_end, _p32(rec))
+            if rc != 0:
+                raise ValueError("rc_oracle_run_chain returned %d" % rc)
+        out = {"state": state, "outcome": outcome, "eff_sid": eff_sid,
+               "eff_tool": eff_tool, "eff_payload": eff_payload, "n_taken": n_taken}
+        if rec is not None:
+            out["decisions"] = rec
+        return out
 
-    def run_inputs(self, inp, n_steps=None, step0=0, cohort_begin=0, cohort_end=None):
+    def run_inputs(self, inp, n_steps=None, step0=0, cohort_begin=0, cohort_end=None,
+                   decisions=None, record=False):
         """Run on a copy of an input bundle from the workload generator."""
         state, outcome = inp.state.copy(), inp.outcome.copy()
         return self.run_chain(
@@ -172,7 +199,8 @@ class Oracle:
             route_mode=inp.route_mode, route_cdf=inp.route_cdf,
             decide_thr=inp.decide_thr, state=state, outcome=outcome,
             n_steps=inp.n_steps if n_steps is None else n_steps, step0=step0,
-            cohort_begin=cohort_begin, cohort_end=cohort_end)
+            cohort_begin=cohort_begin, cohort_end=cohort_end, decisions=decisions,
+            record=record)
 
 
 _default = None

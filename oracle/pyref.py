@@ -42,10 +42,16 @@ def route(o: int, n_routes: int, route_mode: int, cdf=()) -> int:
     return sum(1 for v in cdf if int(v) <= o)
 
 
-def session_step(words, o, step, n_routes, table, route_mode, cdf, thr):
-    """One session's transition: returns (new_words, taken, route, tool)."""
+def session_step(words, o, step, n_routes, table, route_mode, cdf, thr, forced=None):
+    """One session's transition: returns (new_words, taken, route, tool).
+
+    ``forced``: None, or the decision to use instead of the predicate (the
+    no-decision floor replays a recorded decision sequence)."""
     r = route(o, n_routes, route_mode, cdf)
-    taken = (fmix32(words[0] ^ o ^ (step % MOD32)) % 65536) < thr
+    if forced is None:
+        taken = (fmix32(words[0] ^ o ^ (step % MOD32)) % 65536) < thr
+    else:
+        taken = bool(forced)
     if taken:
         new = [x ^ ((int(table[r][w % 16]) * (w + 1)) % MOD32)
                for w, x in enumerate(words)]
@@ -56,11 +62,13 @@ def session_step(words, o, step, n_routes, table, route_mode, cdf, thr):
 
 
 def run_chain(sessions, outcomes, cohorts, n_steps, step0, n_routes, table,
-              route_mode, cdf, thr):
+              route_mode, cdf, thr, forced=None):
     """Chained steps over a list of cohorts.
 
     ``sessions``: dict sid -> list of W words; ``outcomes``: dict sid -> int;
     ``cohorts``: list of lists of sids (each in ascending order).
+    ``forced``: None, or a function (t, sid) -> decision replacing the
+    predicate (the no-decision floor).
     Returns (sessions, outcomes, effects, counts) where ``effects[t][c]`` is
     the list of (sid, tool, payload tuple) in emitted order and
     ``counts[t][c]`` the taken count.
@@ -75,7 +83,8 @@ def run_chain(sessions, outcomes, cohorts, n_steps, step0, n_routes, table,
             results = {}
             for s in members:
                 results[s] = session_step(sessions[s], outcomes[s], step,
-                                          n_routes, table, route_mode, cdf, thr)
+                                          n_routes, table, route_mode, cdf, thr,
+                                          None if forced is None else forced(t, s))
             order = sorted(members, key=lambda s: (not results[s][1], s))
             eff_t.append([(s, results[s][3], tuple(results[s][0][:4])) for s in order])
             cnt_t.append(sum(1 for s in members if results[s][1]))

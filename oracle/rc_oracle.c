@@ -130,25 +130,38 @@ static int check_args(uint32_t n_sessions, uint32_t n_words, uint32_t n_routes,
 }
 
 /*
- * Run T chained steps over the cohorts [cohort_begin, cohort_end).
- * state and outcome are updated in place; effect slices 0..T-1 and
- * n_taken rows 0..T-1 are written.  Sessions of other cohorts and every
- * other element are left untouched.  Returns 0 on success, 1 on invalid
- * arguments, 2 when scratch memory cannot be allocated.
+ * Decision bitmaps ([T][dwords] uint32, dwords = ceil(ld / 32)): bit s mod 32
+ * of word [t][s / 32] is the decision of session s at chained step t.
  */
-int rc_oracle_run_chain(uint32_t n_sessions, uint32_t n_words,
-                        uint32_t n_routes, uint32_t n_cohorts,
-                        const uint32_t *cohort_offsets, const uint32_t *table,
-                        uint32_t route_mode, const uint32_t *route_cdf,
-                        uint32_t decide_thr, uint32_t *state, uint32_t *outcome,
-                        uint32_t *eff_sid, uint32_t *eff_tool,
-                        uint32_t *eff_payload, uint32_t *n_taken, uint32_t ld,
-                        uint32_t step0, uint32_t n_steps,
-                        uint32_t cohort_begin, uint32_t cohort_end)
+static uint32_t bit_of(const uint32_t *bits, uint32_t dwords, uint32_t t,
+                       uint32_t s)
+{
+    return (bits[(size_t)t * dwords + s / 32u] >> (s % 32u)) & 1u;
+}
+
+/*
+ * The chain.  With `forced` NULL every decision comes from the predicate;
+ * otherwise it is read from the bitmap `forced` and no predicate is evaluated
+ * (the no-decision floor of Section 7 "Matched mechanisms": the recorded route
+ * sequence is replayed without predicate or selection).  When `record` is not
+ * NULL the decision of every stepped session is written into that bitmap
+ * (bits of unstepped sessions are left as they are).
+ */
+static int run_core(uint32_t n_sessions, uint32_t n_words, uint32_t n_routes,
+                    uint32_t n_cohorts, const uint32_t *cohort_offsets,
+                    const uint32_t *table, uint32_t route_mode,
+                    const uint32_t *route_cdf, uint32_t decide_thr,
+                    const uint32_t *forced, uint32_t *record,
+                    uint32_t *state, uint32_t *outcome, uint32_t *eff_sid,
+                    uint32_t *eff_tool, uint32_t *eff_payload,
+                    uint32_t *n_taken, uint32_t ld, uint32_t step0,
+                    uint32_t n_steps, uint32_t cohort_begin,
+                    uint32_t cohort_end)
 {
     uint32_t t, c, s, w, q;
     uint32_t *route_of, *taken;
     uint32_t max_size = 0u;
+    const uint32_t dwords = (ld + 31u) / 32u;
 
     if (check_args(n_sessions, n_words, n_routes, n_cohorts, cohort_offsets,
                    table, route_mode, route_cdf, decide_thr, ld, cohort_begin,
@@ -182,7 +195,15 @@ int rc_oracle_run_chain(uint32_t n_sessions, uint32_t n_words,
                 uint32_t o = outcome[s];
                 route_of[s - b] = rc_oracle_route(o, n_routes, route_mode,
                                                   route_cdf);
-                taken[s - b] = rc_oracle_decide(state[s], o, step, decide_thr);
+                if (forced)
+                    taken[s - b] = bit_of(forced, dwords, t, s);
+                else
+                    taken[s - b] = rc_oracle_decide(state[s], o, step, decide_thr);
+                if (record) {
+                    uint32_t *word = &record[(size_t)t * dwords + s / 32u];
+                    *word = (*word & ~(1u << (s % 32u))) |
+                            (taken[s - b] << (s % 32u));
+                }
                 n1 += taken[s - b];
             }
 
@@ -216,6 +237,59 @@ int rc_oracle_run_chain(uint32_t n_sessions, uint32_t n_words,
     free(route_of);
     free(taken);
     return 0;
+}
+
+/*
+ * Run T chained steps over the cohorts [cohort_begin, cohort_end).
+ * state and outcome are updated in place; effect slices 0..T-1 and
+ * n_taken rows 0..T-1 are written.  Sessions of other cohorts and every
+ * other element are left untouched.  decisions_out, when not NULL, is a
+ * [T][ceil(ld/32)] bitmap that receives every stepped session's decision.
+ * Returns 0 on success, 1 on invalid arguments, 2 when scratch memory cannot
+ * be allocated.
+ */
+int rc_oracle_run_chain(uint32_t n_sessions, uint32_t n_words,
+                        uint32_t n_routes, uint32_t n_cohorts,
+                        const uint32_t *cohort_offsets, const uint32_t *table,
+                        uint32_t route_mode, const uint32_t *route_cdf,
+                        uint32_t decide_thr, uint32_t *state, uint32_t *outcome,
+                        uint32_t *eff_sid, uint32_t *eff_tool,
+                        uint32_t *eff_payload, uint32_t *n_taken, uint32_t ld,
+                        uint32_t step0, uint32_t n_steps,
+                        uint32_t cohort_begin, uint32_t cohort_end,
+                        uint32_t *decisions_out)
+{
+    return run_core(n_sessions, n_words, n_routes, n_cohorts, cohort_offsets,
+                    table, route_mode, route_cdf, decide_thr, NULL,
+                    decisions_out, state, outcome, eff_sid, eff_tool,
+                    eff_payload, n_taken, ld, step0, n_steps, cohort_begin,
+                    cohort_end);
+}
+
+/*
+ * The no-decision floor (Section 7 "Matched mechanisms"): the same chain, but
+ * the decision of session s at step t is bit s mod 32 of
+ * decisions[t][s / 32] ([T][ceil(ld/32)] words) and no predicate is
+ * evaluated, so the step number plays no part.  Everything else (routes,
+ * updates, compaction, effects, counts, the chained outcome) is as in
+ * rc_oracle_run_chain.  Same return codes.
+ */
+int rc_oracle_run_floor(uint32_t n_sessions, uint32_t n_words,
+                        uint32_t n_routes, uint32_t n_cohorts,
+                        const uint32_t *cohort_offsets, const uint32_t *table,
+                        uint32_t route_mode, const uint32_t *route_cdf,
+                        const uint32_t *decisions, uint32_t *state,
+                        uint32_t *outcome, uint32_t *eff_sid,
+                        uint32_t *eff_tool, uint32_t *eff_payload,
+                        uint32_t *n_taken, uint32_t ld, uint32_t n_steps,
+                        uint32_t cohort_begin, uint32_t cohort_end)
+{
+    if (!decisions)
+        return 1;
+    return run_core(n_sessions, n_words, n_routes, n_cohorts, cohort_offsets,
+                    table, route_mode, route_cdf, 0u, decisions, NULL, state,
+                    outcome, eff_sid, eff_tool, eff_payload, n_taken, ld, 0u,
+                    n_steps, cohort_begin, cohort_end);
 }
 
 /* Count, over every one of the 2^32 outcomes o, the sessions that would be

@@ -426,7 +426,15 @@ struct ChainArgs {
     uint32_t cohort_begin, cohort_end;
     uint32_t bins_a_lo, bins_a_n, bins_b_lo, bins_b_n;  // sub-wave / multi-wave bins
     uint32_t img_words, tools_off, cdf_off, guide_off;  // in words
+    const uint32_t* dbits;  // no-decision floor: [T][dwords] decision bitmap
+    uint32_t dwords;
 };
+
+// No-decision floor: the bitmap word holding session s's decision at chained
+// step t (bit s mod 32).  Idle lanes read session 0's word.
+__device__ __forceinline__ uint32_t dword_of(const ChainArgs& a, uint32_t t, uint32_t s) {
+    return a.dbits[(size_t)t * a.dwords + (s >> 5)];
+}
 
 // One row (WM words) of the image; logical block q of row r sits at block
 // q ^ (r mod NB), so its byte address is one XOR away.
@@ -487,7 +495,9 @@ __device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[1
 // 64 sessions (every non-empty wavefront is part of one), so each step
 // exchanges popcounts behind a workgroup barrier; otherwise every cohort lies
 // inside one wavefront and no barrier is needed.
-template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool MULTI>
+// FLOOR: the no-decision floor -- every decision is read from the bitmap
+// (prefetched a step ahead) instead of computed; nothing else changes.
+template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool MULTI, bool FLOOR>
 struct Chain {
     static constexpr int MW = FULL ? WMAX : 16;
     // Effect stores are nontemporal here: this path serves the large
@@ -500,6 +510,7 @@ struct Chain {
     struct Lane {
         uint32_t S[WMAX];
         uint32_t o, r, step, pub;
+        uint32_t dw;  // FLOOR: bitmap word of the next step to decide
         bool dk;
         uint64_t bal;
         uint32_t c4[4];
@@ -539,7 +550,13 @@ struct Chain {
         // (a8) chain: next outcome; (a3, a4) the next step's route and decision
         const uint32_t o_n = dev_fmix32(st.S[0]);
         const uint32_t r_n = route_of<RK>(o_n, a.ra, lds + a.cdf_off, lds + a.guide_off);
-        const bool d_n = L.active && ((dev_fmix32(st.S[0] ^ o_n ^ (st.step + 1u)) & 0xFFFFu) < a.thr);
+        bool d_n;
+        if constexpr (FLOOR) {
+            d_n = L.active && ((st.dw >> (L.s & 31u)) & 1u);
+            if (t + 2u < a.n_steps) st.dw = dword_of(a, t + 2u, L.active ? L.s : 0u);
+        } else {
+            d_n = L.active && ((dev_fmix32(st.S[0] ^ o_n ^ (st.step + 1u)) & 0xFFFFu) < a.thr);
+        }
         const uint64_t bal_n = __ballot(d_n);
         if constexpr (MULTI) publish_count(L, bal_n, lane, wv, lds_cnt, CNT_STRIDE, st.pub);
         if constexpr (FULL) load_row<MW>(lds, d_n ? r_n : R, mn);
@@ -648,18 +665,29 @@ struct Chain {
 #pragma unroll
         for (int w = 0; w < WMAX; ++w) st.S[w] = 0;
         st.o = 0;
+        uint32_t dw0 = 0u;
+        st.dw = 0u;
+        if constexpr (FLOOR) {
+            // the first two steps' decision words, ahead of the state words
+            const uint32_t ls = L.active ? L.s : 0u;
+            dw0 = dword_of(a, 0u, ls);
+            if (T > 1u) st.dw = dword_of(a, 1u, ls);
+        }
         if (L.active) {
             const uint32_t ldw = opaque_s(a.ld);
+            st.o = ld32(a.outcome, soff);
 #pragma unroll
             for (int w = 0; w < WMAX; ++w)
                 if (EXACT || (uint32_t)w < W) st.S[w] = ld32(a.state + (size_t)w * ldw, soff);
-            st.o = ld32(a.outcome, soff);
         }
 
         // decision of the first step
         st.step = a.step0;
         st.r = route_of<RK>(st.o, a.ra, lds + a.cdf_off, lds + a.guide_off);
-        st.dk = L.active && ((dev_fmix32(st.S[0] ^ st.o ^ st.step) & 0xFFFFu) < a.thr);
+        if constexpr (FLOOR)
+            st.dk = L.active && ((dw0 >> (L.s & 31u)) & 1u);
+        else
+            st.dk = L.active && ((dev_fmix32(st.S[0] ^ st.o ^ st.step) & 0xFFFFu) < a.thr);
         st.bal = __ballot(st.dk);
 #pragma unroll
         for (int k = 0; k < 4; ++k) st.c4[k] = 0u;
@@ -708,7 +736,9 @@ struct Chain {
 // Rows of the mask image are W + 4 words apart (one zero block of padding
 // shifts consecutive rows across the LDS banks), so block q of a row is an
 // immediate offset from the row's byte offset.
-template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT>
+// FLOOR: the no-decision floor -- the A lanes read every decision from the
+// bitmap (each chunk's words loaded a chunk ahead) instead of computing it.
+template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT, bool FLOOR>
 struct ChainF {
     // Effect stores stay on the normal path: cohorts spanning wavefronts
     // fill each line from several wavefronts.
@@ -764,6 +794,18 @@ struct ChainF {
         const uint32_t loff = L.active ? soff : 0u;
         const uint32_t ldw = opaque_s(a.ld);
         uint32_t o = ld32(a.outcome, loff);
+        // FLOOR: the decision words of the first chunk (A lanes), issued
+        // before the state words so that the chain waits only for word 0
+        uint32_t db[TC];
+#pragma unroll
+        for (int i = 0; i < TC; ++i) db[i] = 0u;
+        if constexpr (FLOOR) {
+            if (!role_b) {
+#pragma unroll
+                for (int i = 0; i < TC; ++i)
+                    if ((uint32_t)i < T) db[i] = dword_of(a, (uint32_t)i, L.active ? L.s : 0u);
+            }
+        }
 #pragma unroll
         for (int w = 0; w < WH; ++w)
             S[w] = (EXACT || wbase + (uint32_t)w < W) ? ld32(a.state + (size_t)(wbase + w) * ldw, loff) : 0u;
@@ -790,6 +832,17 @@ struct ChainF {
             }
         }
 
+        // FLOOR: this chunk's decisions packed into one register (bit i =
+        // step t0 + i), so the words die as soon as they arrive
+        auto pack = [&](const uint32_t (&w)[TC]) {
+            uint32_t m = 0u;
+#pragma unroll
+            for (int i = 0; i < TC; ++i) m |= ((w[i] >> (L.s & 31u)) & 1u) << i;
+            return L.active ? m : 0u;
+        };
+        uint32_t dm = 0u;
+        if constexpr (FLOOR) dm = pack(db);
+
         uint32_t s0 = S[0];  // word 0 of the chain (A lanes)
         uint32_t step = a.step0;
         uint32_t* p_sid = a.eff_sid;
@@ -807,13 +860,19 @@ struct ChainF {
             }
 
             if (!role_b) {
+                if constexpr (FLOOR)
+                    if (t0 != 0u) dm = pack(db);
                 // chain: word 0 only
                 uint32_t r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
                 uint32_t m0 = lds[__umul24(r, RS) >> 2];  // taken mask of word 0, row r
 #pragma unroll
                 for (int i = 0; i < TC; ++i) {
                     if ((uint32_t)i >= n) continue;
-                    const bool dk = L.active && ((dev_fmix32(s0 ^ o ^ step) & 0xFFFFu) < a.thr);
+                    bool dk;
+                    if constexpr (FLOOR)
+                        dk = (dm >> i) & 1u;
+                    else
+                        dk = L.active && ((dev_fmix32(s0 ^ o ^ step) & 0xFFFFu) < a.thr);
                     const uint32_t sh = (31u - r) & 31u;
                     const uint32_t oo = opaque(dk ? 0u : o);
                     ctl[i] = (dk ? 32u : sh) | (r << 6);  // rotation 0 when taken
@@ -823,6 +882,15 @@ struct ChainF {
                     r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
                     m0 = lds[__umul24(r, RS) >> 2];
                     step += 1u;
+                }
+                // FLOOR: the next chunk's decision words, in flight during
+                // this chunk's replay
+                if constexpr (FLOOR) {
+                    if (t0 + (uint32_t)TC < T) {
+#pragma unroll
+                        for (int i = 0; i < TC; ++i)
+                            db[i] = t0 + (uint32_t)(TC + i) < T ? dword_of(a, t0 + TC + i, L.active ? L.s : 0u) : 0u;
+                    }
                 }
                 // counts of the chunk's steps: every lane writes the same
                 // (uniform) value to the same address, so no lane mask
@@ -955,23 +1023,25 @@ struct ChainF {
 };
 
 // One workgroup per bin: blocks [0, bins_a_n) take the sub-wavefront bins,
-// the rest the multi-wavefront bins.  The table-image variant runs two
-// 512-lane workgroups per CU, so it is held to four wavefronts per SIMD.
-template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK>
-__global__ __launch_bounds__((FULL && WMAX >= 32 ? 2 : 1) * NWAVE * 64, FULL ? 1 : 4)
+// the rest the multi-wavefront bins.  The table-image chain and the two-lane
+// full-image chain at W <= 32 run two 512-lane workgroups per CU, so they are
+// held to four wavefronts per SIMD (at most 128 VGPRs).  At W = 64 the
+// two-lane full-image chain needs more registers and runs one per CU.
+template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool FLOOR>
+__global__ __launch_bounds__((FULL && WMAX >= 32 ? 2 : 1) * NWAVE * 64, (!FULL || WMAX == 32) ? 4 : 1)
 void rc_chain_kernel(ChainArgs a) {
     extern __shared__ uint4 lds4[];
     if constexpr (FULL) {
         constexpr bool SPLIT = WMAX >= 32;
         if (blockIdx.x < a.bins_a_n)
-            ChainF<WMAX, EXACT, NWAVE, RK, false, SPLIT>::run(a, a.bins_a_lo + blockIdx.x, lds4);
+            ChainF<WMAX, EXACT, NWAVE, RK, false, SPLIT, FLOOR>::run(a, a.bins_a_lo + blockIdx.x, lds4);
         else
-            ChainF<WMAX, EXACT, NWAVE, RK, true, SPLIT>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
+            ChainF<WMAX, EXACT, NWAVE, RK, true, SPLIT, FLOOR>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
     } else {
         if (blockIdx.x < a.bins_a_n)
-            Chain<WMAX, EXACT, NWAVE, FULL, RK, false>::run(a, a.bins_a_lo + blockIdx.x, lds4);
+            Chain<WMAX, EXACT, NWAVE, FULL, RK, false, FLOOR>::run(a, a.bins_a_lo + blockIdx.x, lds4);
         else
-            Chain<WMAX, EXACT, NWAVE, FULL, RK, true>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
+            Chain<WMAX, EXACT, NWAVE, FULL, RK, true, FLOOR>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
     }
 }
 
@@ -1097,30 +1167,35 @@ typedef void (*ChainFn)(ChainArgs);
 typedef void (*DecideFn)(DecideArgs);
 typedef void (*BodyFn)(BodyArgs);
 
-template <int WMAX, bool EXACT, int RK>
+template <int WMAX, bool EXACT, int RK, bool FLOOR>
 ChainFn chain_fn(bool full) {
     if (!full) {
-        if constexpr (WMAX >= 32) return rc_chain_kernel<WMAX, EXACT, 8, false, RK>;
+        if constexpr (WMAX >= 32) return rc_chain_kernel<WMAX, EXACT, 8, false, RK, FLOOR>;
         return nullptr;
     }
-    return rc_chain_kernel<WMAX, EXACT, 4, true, RK>;
+    return rc_chain_kernel<WMAX, EXACT, 4, true, RK, FLOOR>;
 }
 
-template <int WMAX, bool EXACT>
+template <int WMAX, bool EXACT, bool FLOOR>
 ChainFn chain_fn_rk(bool full, int rk) {
-    return rk == RK_POW2 ? chain_fn<WMAX, EXACT, RK_POW2>(full)
-         : rk == RK_MOD ? chain_fn<WMAX, EXACT, RK_MOD>(full)
-                        : chain_fn<WMAX, EXACT, RK_CDF>(full);
+    return rk == RK_POW2 ? chain_fn<WMAX, EXACT, RK_POW2, FLOOR>(full)
+         : rk == RK_MOD ? chain_fn<WMAX, EXACT, RK_MOD, FLOOR>(full)
+                        : chain_fn<WMAX, EXACT, RK_CDF, FLOOR>(full);
 }
 
-ChainFn pick_chain(uint32_t wmax, bool exact, bool full, int rk) {
+template <bool FLOOR>
+ChainFn pick_chain_t(uint32_t wmax, bool exact, bool full, int rk) {
     switch (wmax) {
-        case 4: return exact ? chain_fn_rk<4, true>(full, rk) : chain_fn_rk<4, false>(full, rk);
-        case 8: return exact ? chain_fn_rk<8, true>(full, rk) : chain_fn_rk<8, false>(full, rk);
-        case 16: return exact ? chain_fn_rk<16, true>(full, rk) : chain_fn_rk<16, false>(full, rk);
-        case 32: return exact ? chain_fn_rk<32, true>(full, rk) : chain_fn_rk<32, false>(full, rk);
-        default: return exact ? chain_fn_rk<64, true>(full, rk) : chain_fn_rk<64, false>(full, rk);
+        case 4: return exact ? chain_fn_rk<4, true, FLOOR>(full, rk) : chain_fn_rk<4, false, FLOOR>(full, rk);
+        case 8: return exact ? chain_fn_rk<8, true, FLOOR>(full, rk) : chain_fn_rk<8, false, FLOOR>(full, rk);
+        case 16: return exact ? chain_fn_rk<16, true, FLOOR>(full, rk) : chain_fn_rk<16, false, FLOOR>(full, rk);
+        case 32: return exact ? chain_fn_rk<32, true, FLOOR>(full, rk) : chain_fn_rk<32, false, FLOOR>(full, rk);
+        default: return exact ? chain_fn_rk<64, true, FLOOR>(full, rk) : chain_fn_rk<64, false, FLOOR>(full, rk);
     }
+}
+
+ChainFn pick_chain(uint32_t wmax, bool exact, bool full, int rk, bool floor) {
+    return floor ? pick_chain_t<true>(wmax, exact, full, rk) : pick_chain_t<false>(wmax, exact, full, rk);
 }
 
 template <int WMAX, bool EXACT>
@@ -1390,29 +1465,34 @@ bool device_extent_ok(const void* p, size_t bytes, int dev) {
     return q >= b && q - b <= size && bytes <= size - (q - b);
 }
 
-int validate_buffers(const rc_cohort* h, const rc_buffers* b, uint32_t T) {
+// The caller's buffers (and, for the no-decision floor, its decision
+// bitmap): present, inside one device allocation each, pairwise disjoint.
+int validate_buffers(const rc_cohort* h, const rc_buffers* b, uint32_t T, bool floor = false,
+                     const uint32_t* dbits = nullptr) {
     if (!b) return RC_E_INVALID;
     if (b->ld < h->N || b->ld > RC_MAX_SESSIONS) return RC_E_INVALID;
     const uint64_t ld = b->ld;
-    struct Ext { const void* p; uint64_t bytes; } ext[6] = {
+    struct Ext { const void* p; uint64_t bytes; } ext[7] = {
         {b->state, 4ull * h->W * ld},
         {b->outcome, 4ull * ld},
         {b->eff_sid, 4ull * T * ld},
         {b->eff_tool, 4ull * T * ld},
         {b->eff_payload, 16ull * T * ld},
         {b->n_taken, 4ull * T * h->C},
+        {dbits, 4ull * T * ((ld + 31u) / 32u)},
     };
-    for (int i = 0; i < 6; ++i) {
+    const int n = floor ? 7 : 6;
+    for (int i = 0; i < n; ++i) {
         if (!ext[i].p) return RC_E_INVALID;
         if (ext[i].bytes >= (1ull << 46)) return RC_E_INVALID;
     }
-    for (int i = 0; i < 6; ++i)
-        for (int j = i + 1; j < 6; ++j) {
+    for (int i = 0; i < n; ++i)
+        for (int j = i + 1; j < n; ++j) {
             const uintptr_t a0 = (uintptr_t)ext[i].p, a1 = a0 + ext[i].bytes;
             const uintptr_t b0 = (uintptr_t)ext[j].p, b1 = b0 + ext[j].bytes;
             if (a0 < b1 && b0 < a1) return RC_E_INVALID;
         }
-    for (int i = 0; i < 6; ++i)
+    for (int i = 0; i < n; ++i)
         if (ext[i].bytes && !device_extent_ok(ext[i].p, ext[i].bytes, h->device)) return RC_E_INVALID;
     return RC_OK;
 }
@@ -1422,7 +1502,7 @@ int launch_ok() {
 }
 
 int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
-                 uint32_t cb, uint32_t ce, hipStream_t stream) {
+                 uint32_t cb, uint32_t ce, hipStream_t stream, const uint32_t* dbits = nullptr) {
     ChainArgs a;
     a.state = b->state;
     a.outcome = b->outcome;
@@ -1447,8 +1527,10 @@ int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
     a.tools_off = h->tools_off;
     a.cdf_off = h->cdf_off;
     a.guide_off = h->guide_off;
+    a.dbits = dbits;
+    a.dwords = (b->ld + 31u) / 32u;
     const uint32_t grid = a.bins_a_n + a.bins_b_n;  // one workgroup per bin
-    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind);
+    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind, dbits != nullptr);
     hipLaunchKernelGGL(fn, dim3(grid), dim3(h->chain_threads), h->chain_lds_bytes, stream, a);
     if (launch_ok() != RC_OK) return RC_E_DEVICE;
     h->last_launches = 1;
@@ -1658,8 +1740,8 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
         h->ra.guide_top = 0;
         while (span && (h->ra.guide_top << 1) <= span) h->ra.guide_top = h->ra.guide_top ? h->ra.guide_top << 1 : 1u;
     }
-    if (rc == RC_OK) {
-        ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind);
+    for (int fl = 0; fl < 2 && rc == RC_OK; ++fl) {
+        ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind, fl != 0);
         if (!fn) rc = RC_E_DEVICE;
         if (rc == RC_OK && hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                                (int)h->chain_lds_bytes) != hipSuccess) rc = RC_E_DEVICE;
@@ -1688,6 +1770,20 @@ int rc_cohort_run_chain(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint3
     hipStream_t stream = (hipStream_t)hip_stream;
     if (mode == RC_MODE_RESIDENT) return run_resident(h, b, step0, n_steps, cohort_begin, cohort_end, stream);
     return run_host_roundtrip(h, b, step0, n_steps, cohort_begin, cohort_end, stream);
+}
+
+int rc_cohort_run_floor(rc_cohort* h, const rc_buffers* b, const uint32_t* decisions, uint32_t n_steps,
+                        uint32_t cohort_begin, uint32_t cohort_end, void* hip_stream) {
+    if (!h || !b || !decisions) return RC_E_INVALID;
+    if (cohort_begin > cohort_end || cohort_end > h->C) return RC_E_INVALID;
+    DeviceGuard guard(h->device);
+    if (!guard.ok) return RC_E_DEVICE;
+    const int v = validate_buffers(h, b, n_steps, true, decisions);
+    if (v != RC_OK) return v;
+    h->last_launches = 0;
+    h->last_d2h = 0;
+    if (n_steps == 0u || cohort_begin == cohort_end) return RC_OK;
+    return run_resident(h, b, 0u, n_steps, cohort_begin, cohort_end, (hipStream_t)hip_stream, decisions);
 }
 
 int rc_cohort_step(rc_cohort* h, const rc_buffers* b, uint32_t step, uint32_t cohort_begin,

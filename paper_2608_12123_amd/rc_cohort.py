@@ -25,8 +25,9 @@ RC_ROUTE_MOD, RC_ROUTE_CDF = 0, 1
 RC_MODE_RESIDENT, RC_MODE_HOST_ROUNDTRIP = 0, 1
 
 EXPORTED = [
-    "rc_cohort_create", "rc_cohort_step", "rc_cohort_run_chain", "rc_cohort_destroy",
-    "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info", "rc_plan_lanes",
+    "rc_cohort_create", "rc_cohort_step", "rc_cohort_run_chain", "rc_cohort_run_floor",
+    "rc_cohort_destroy", "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info",
+    "rc_plan_lanes",
 ]
 
 _P32 = ctypes.POINTER(ctypes.c_uint32)
@@ -87,6 +88,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.c_uint32, ctypes.c_int, ctypes.c_uint32,
                                         ctypes.c_uint32, ctypes.c_void_p]
     lib.rc_cohort_run_chain.restype = ctypes.c_int
+    lib.rc_cohort_run_floor.argtypes = [ctypes.c_void_p, ctypes.POINTER(RcBuffers), ctypes.c_void_p,
+                                        ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                                        ctypes.c_void_p]
+    lib.rc_cohort_run_floor.restype = ctypes.c_int
     lib.rc_cohort_destroy.argtypes = [ctypes.c_void_p]
     lib.rc_cohort_destroy.restype = ctypes.c_int
     lib.rc_status_string.argtypes = [ctypes.c_int]
@@ -163,6 +168,17 @@ def rc_cohort_run_chain(h, buffers: RcBuffers, step0: int, n_steps: int, mode: i
                                             _stream_handle(stream))
     if check:
         _check(st, "rc_cohort_run_chain")
+    return st
+
+
+def rc_cohort_run_floor(h, buffers: RcBuffers, decisions_ptr: int, n_steps: int,
+                        cohort_begin: int, cohort_end: int, stream=None, check: bool = True) -> int:
+    """The no-decision floor; ``decisions_ptr`` is the device address of a
+    ``[n_steps][ceil(ld/32)]`` uint32 decision bitmap."""
+    st = load_library().rc_cohort_run_floor(h, ctypes.byref(buffers), decisions_ptr, n_steps,
+                                            cohort_begin, cohort_end, _stream_handle(stream))
+    if check:
+        _check(st, "rc_cohort_run_floor")
     return st
 
 
@@ -267,6 +283,18 @@ class Cohort:
         ce = self.n_cohorts if cohort_end is None else cohort_end
         return rc_cohort_run_chain(self.handle, self.buffers, step0, n_steps, mode, cohort_begin,
                                    ce, stream)
+
+    def run_floor(self, decisions: np.ndarray, n_steps, cohort_begin=0, cohort_end=None,
+                  stream=None):
+        """The no-decision floor with a host ``[n_steps][ceil(ld/32)]`` uint32
+        decision bitmap (uploaded to the device first)."""
+        assert n_steps <= self.max_steps
+        bits = np.ascontiguousarray(decisions, dtype=np.uint32)
+        assert bits.shape == (n_steps, (self.ld + 31) // 32)
+        self.t_bits = _to_device_u32(bits, self.device)
+        ce = self.n_cohorts if cohort_end is None else cohort_end
+        return rc_cohort_run_floor(self.handle, self.buffers, self.t_bits.data_ptr(), n_steps,
+                                   cohort_begin, ce, stream)
 
     def step(self, step, cohort_begin=0, cohort_end=None, stream=None):
         ce = self.n_cohorts if cohort_end is None else cohort_end

@@ -91,7 +91,7 @@ def rotl_closed(x: int, k: int) -> int:
 
 
 def single_run(oracle, *, words, outcomes, table, thr, n_routes, route_mode=ROUTE_MOD,
-               cdf=None, n_steps=1, step0=0, sizes=None, ld=None):
+               cdf=None, n_steps=1, step0=0, sizes=None, ld=None, decisions=None, record=False):
     """Run the oracle over sessions whose initial words/outcomes are given.
 
     ``words``: [N][W] python ints; ``outcomes``: [N]."""
@@ -107,7 +107,8 @@ def single_run(oracle, *, words, outcomes, table, thr, n_routes, route_mode=ROUT
     return oracle.run_chain(n_words=W, n_routes=n_routes, cohort_offsets=offsets,
                             table=np.asarray(table, dtype=np.uint32).reshape(n_routes, 16),
                             route_mode=route_mode, route_cdf=cdf, decide_thr=thr,
-                            state=state, outcome=outcome, n_steps=n_steps, step0=step0)
+                            state=state, outcome=outcome, n_steps=n_steps, step0=step0,
+                            decisions=decisions, record=record)
 
 
 def rand_u32(n, seed):
@@ -514,6 +515,110 @@ def pin_brute_force_cohorts(oracle):
                 assert res["n_taken"][t, c] == p_c[t][c]
 
 
+# --------------------------------------------------------------------------
+# pins: the no-decision floor (Section 7 "Matched mechanisms": the recorded
+# route sequence replayed without predicate or selection)
+# --------------------------------------------------------------------------
+def bits_from_bool(dec):
+    """[T][ld] booleans -> [T][ceil(ld/32)] uint32 bitmap, bit s mod 32 of
+    word s // 32 (written with plain Python integers)."""
+    T, ld = len(dec), len(dec[0])
+    out = np.zeros((T, (ld + 31) // 32), dtype=np.uint32)
+    for t in range(T):
+        for s in range(ld):
+            if dec[t][s]:
+                out[t, s // 32] = int(out[t, s // 32]) | (1 << (s % 32))
+    return out
+
+
+def pin_floor_replays_recorded(oracle):
+    """The chain's recorded decisions replayed through the floor give the
+    chain's outputs; the record agrees with the pinned decision rule and with
+    the taken counts."""
+    sizes = [5, 32, 33, 64, 70]
+    N, W, R, ld = sum(sizes), 6, 7, sum(sizes) + 9
+    words = rand_u32(N * W, 301).reshape(N, W).tolist()
+    outs = rand_u32(N, 302).tolist()
+    table = rand_u32(R * 16, 303).reshape(R, 16)
+    base = single_run(oracle, words=words, outcomes=outs, table=table, thr=30000, n_routes=R,
+                      sizes=sizes, ld=ld, n_steps=4, step0=11)
+    rec = single_run(oracle, words=words, outcomes=outs, table=table, thr=30000, n_routes=R,
+                     sizes=sizes, ld=ld, n_steps=1, step0=11, record=True)["decisions"]
+    for s in range(N):
+        want = _decisions_by_pinned_rule(oracle, words[s][0], outs[s], 11, 30000)
+        assert ((int(rec[0, s // 32]) >> (s % 32)) & 1) == want
+    for s in range(N, ld):  # sessions past N are never stepped
+        assert ((int(rec[0, s // 32]) >> (s % 32)) & 1) == 0
+    full = single_run(oracle, words=words, outcomes=outs, table=table, thr=30000, n_routes=R,
+                      sizes=sizes, ld=ld, n_steps=4, step0=11, record=True)
+    flo = single_run(oracle, words=words, outcomes=outs, table=table, thr=0, n_routes=R,
+                     sizes=sizes, ld=ld, n_steps=4, step0=999, decisions=full["decisions"])
+    for k in base:
+        assert np.array_equal(base[k], flo[k]), k
+    offs = np.concatenate([[0], np.cumsum(sizes)])
+    for t in range(4):
+        for c in range(len(sizes)):
+            n = sum((int(full["decisions"][t, s // 32]) >> (s % 32)) & 1 for s in range(offs[c], offs[c + 1]))
+            assert n == int(base["n_taken"][t, c])
+
+
+def pin_floor_against_pyref(oracle):
+    """Random decision bitmaps (every cohort size class, both route maps)
+    against the Python formulation with the same forced decisions."""
+    sizes = [1, 3, 31, 32, 33, 64, 65, 129, 256]
+    N, W, R, T = sum(sizes), 5, 6, 3
+    ld = N + 5
+    words = rand_u32(N * W, 311).reshape(N, W)
+    outs = rand_u32(N, 312)
+    table = rand_u32(R * 16, 313).reshape(R, 16)
+    cdf = np.asarray([7, 1 << 27, 1 << 30, 3 << 30, 0xFFFFFFF0], dtype=np.uint32)
+    rng = np.random.Generator(np.random.PCG64(314))
+    dec = (rng.random((T, ld)) < 0.37).tolist()
+    bits = bits_from_bool(dec)
+    offs = np.concatenate([[0], np.cumsum(sizes)])
+    cohorts = [list(range(offs[c], offs[c + 1])) for c in range(len(sizes))]
+    for mode in (ROUTE_MOD, ROUTE_CDF):
+        res = single_run(oracle, words=words.tolist(), outcomes=outs.tolist(), table=table,
+                         thr=12345, n_routes=R, route_mode=mode, cdf=cdf if mode == ROUTE_CDF else None,
+                         sizes=sizes, n_steps=T, ld=ld, decisions=bits)
+        p_s, p_o, p_e, p_c = pyref.run_chain(
+            {i: words[i].tolist() for i in range(N)}, {i: int(outs[i]) for i in range(N)},
+            cohorts, T, 0, R, table.tolist(), mode, cdf.tolist() if mode == ROUTE_CDF else [],
+            12345, forced=lambda t, s: dec[t][s])
+        assert res["state"][:, :N].T.tolist() == [p_s[i] for i in range(N)]
+        assert res["outcome"][:N].tolist() == [p_o[i] for i in range(N)]
+        for t in range(T):
+            for c in range(len(sizes)):
+                e = p_e[t][c]
+                sl = slice(offs[c], offs[c + 1])
+                assert res["eff_sid"][t, sl].tolist() == [x[0] for x in e]
+                assert res["eff_tool"][t, sl].tolist() == [x[1] for x in e]
+                assert res["eff_payload"][t, sl, :].tolist() == [list(x[2]) for x in e]
+                assert res["n_taken"][t, c] == p_c[t][c]
+
+
+def pin_floor_closed_forms(oracle):
+    """All taken on one route: two steps XOR the same masks, so the state
+    returns after every even number of steps whatever the threshold, and
+    every session is counted; none taken with outcome 0 for one step: every
+    word is rotated left by 1."""
+    N, W, ld = 70, 8, 96
+    words = rand_u32(N * W, 321).reshape(N, W).tolist()
+    outs = rand_u32(N, 322).tolist()
+    table = rand_u32(16, 323).reshape(1, 16)
+    ones = np.full((4, ld // 32), 0xFFFFFFFF, dtype=np.uint32)
+    res = single_run(oracle, words=words, outcomes=outs, table=table, thr=0, n_routes=1,
+                     n_steps=4, ld=ld, decisions=ones)
+    assert res["state"][:, :N].T.tolist() == words
+    assert res["n_taken"][:, 0].tolist() == [N] * 4
+    assert res["eff_sid"][:, :N].tolist() == [list(range(N))] * 4
+    zeros = np.zeros((1, ld // 32), dtype=np.uint32)
+    res = single_run(oracle, words=words, outcomes=[0] * N, table=table, thr=65536, n_routes=1,
+                     n_steps=1, ld=ld, decisions=zeros)
+    assert res["state"][:, :N].T.tolist() == [[rotl_closed(x, 1) for x in w] for w in words]
+    assert res["n_taken"][0, 0] == 0
+
+
 QUICK_PINS = [
     pin_fmix32_vectors, pin_rotl_closed_form, pin_route_mod, pin_route_cdf,
     pin_decide_known_answers, pin_taken_unit_table, pin_taken_single_column,
@@ -521,4 +626,5 @@ QUICK_PINS = [
     pin_cdf_route_in_chain, pin_tool_column, pin_decide_uses_pre_update_state_and_step,
     pin_payload_post_update, pin_stable_partition, pin_chain_invariants,
     pin_untouched_outside_range, pin_chain_composes, pin_replay_deterministic,
+    pin_floor_replays_recorded, pin_floor_against_pyref, pin_floor_closed_forms,
 ]

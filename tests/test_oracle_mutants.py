@@ -50,6 +50,16 @@ MUTANTS = {
                         "n_taken[(size_t)t * n_cohorts + c] = (e - b) - n1;"),
     "sid_relative": ("eff_sid[slice + slot] = s;", "eff_sid[slice + slot] = s - b;"),
     "slice_unshifted": ("size_t slice = (size_t)t * ld;", "size_t slice = 0;"),
+    "floor_bit_shifted": ("return (bits[(size_t)t * dwords + s / 32u] >> (s % 32u)) & 1u;",
+                          "return (bits[(size_t)t * dwords + s / 32u] >> ((s + 1u) % 32u)) & 1u;"),
+    "floor_row_stride": ("return (bits[(size_t)t * dwords + s / 32u] >> (s % 32u)) & 1u;",
+                         "return (bits[(size_t)t * (dwords - 1u) + s / 32u] >> (s % 32u)) & 1u;"),
+    "floor_dwords_floor": ("const uint32_t dwords = (ld + 31u) / 32u;", "const uint32_t dwords = ld / 32u + 1u;"),
+    "floor_inverted": ("taken[s - b] = bit_of(forced, dwords, t, s);",
+                       "taken[s - b] = 1u - bit_of(forced, dwords, t, s);"),
+    "floor_ignored": ("        if (forced)\n", "        if (0)\n"),
+    "record_step_zero": ("uint32_t *word = &record[(size_t)t * dwords + s / 32u];",
+                         "uint32_t *word = &record[s / 32u];"),
 }
 
 
