@@ -361,6 +361,7 @@ struct ImageArgs {
     uint32_t* max_span;   // out: largest guide bucket span
     uint32_t n_routes, row_words, full, tab_words, tools_off, cdf_off, cdf_n;
     uint32_t guide_off, guide_n, guide_shift, total_words;
+    uint32_t m0_words, rows_off;  // full image: word-0 masks at 0, rows at rows_off
 };
 
 // number of thresholds <= x (plain binary search over global memory)
@@ -378,14 +379,19 @@ __global__ __launch_bounds__(256) void rc_prep_kernel(ImageArgs a) {
     if (i >= a.total_words) return;
     const uint32_t R = a.n_routes;
     uint32_t v = 0;
-    if (i < a.tab_words) {
+    if (a.full && i < a.m0_words) {
+        // word 0's taken mask of route i (row R and the padding: zero)
+        if (i < R) v = a.raw[i * 16u];
+    } else if (i >= a.rows_off && i < a.rows_off + a.tab_words) {
+        const uint32_t j = i - a.rows_off;
         if (a.full) {
             // row r: W masks, then one zero block of padding
             const uint32_t WM = a.row_words, RS = WM + 4u;
-            const uint32_t r = i / RS, w = i % RS;
+            const uint32_t r = j / RS, w = j % RS;
             if (r < R && w < WM) v = a.raw[r * 16u + (w & 15u)] * (w + 1u);
         } else {
-            const uint32_t r = i / 16u, p = i % 16u;
+            const uint32_t i2 = j;
+            const uint32_t r = i2 / 16u, p = i2 % 16u;
             const uint32_t q = (p >> 2) ^ (r & 3u);
             const uint32_t w = 4u * q + (p & 3u);
             if (r < R) v = a.raw[r * 16u + w];
@@ -426,6 +432,8 @@ struct ChainArgs {
     uint32_t cohort_begin, cohort_end;
     uint32_t bins_a_lo, bins_a_n, bins_b_lo, bins_b_n;  // sub-wave / multi-wave bins
     uint32_t img_words, tools_off, cdf_off, guide_off;  // in words
+    uint32_t rows_off;     // full image: first word of the mask rows
+    uint32_t chain_words;  // full image: words [0, chain_words) are what the word-0 chain reads
     const uint32_t* dbits;  // no-decision floor: [T][dwords] decision bitmap
     uint32_t dwords;
 };
@@ -771,53 +779,118 @@ struct ChainF {
         uint32_t* lds_x = lds_cnt + TC * CNT_STRIDE;    // SPLIT: [TC][2][NWAVE * 64]
         const uint32_t* lds_tools = lds + a.tools_off;
 
-        // (a1, a2) the lane's descriptor first (scalar loads), then the first
-        // batch of the table image, then the outcome and the state words.
-        // Vector-memory loads complete in order, so the image batch can be
-        // written to LDS while the state loads are still in flight.
+        const uint32_t* lds_rows = lds + a.rows_off;
         const LaneCohort L = lane_cohort(a.wdesc + ((size_t)bin * NWAVE + wa) * WD_WORDS,
                                          a.offsets, lane, a.cohort_begin, a.cohort_end);
         const uint32_t soff = L.s << 2;
         typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
         const u32x4* src = reinterpret_cast<const u32x4*>(a.img);
-        u32x4* dst = reinterpret_cast<u32x4*>(lds4);
         const uint32_t n4 = a.img_words / 4u;
-        u32x4 v[SB];
-#pragma unroll
-        for (int k = 0; k < SB; ++k) {
-            const uint32_t j = tid + (uint32_t)k * WG;
-            v[k] = src[j < n4 ? j : n4 - 1u];
-        }
         // Unconditional loads (idle lanes read session 0 and never store), so
         // that no branch splits the in-order load sequence.
         uint32_t S[WH];
         const uint32_t loff = L.active ? soff : 0u;
         const uint32_t ldw = opaque_s(a.ld);
-        uint32_t o = ld32(a.outcome, loff);
-        // FLOOR: the decision words of the first chunk (A lanes), issued
-        // before the state words so that the chain waits only for word 0
-        uint32_t db[TC];
+        uint32_t o = 0u;
+        // Word 0 of the chain (A lanes) in a variable of its own: on the B
+        // path it is a constant, so no wait for outstanding state loads is
+        // attached to it where the two paths join.
+        uint32_t s0 = 0u;
+        uint32_t db[TC];  // FLOOR: the decision words of the first chunk (A lanes)
 #pragma unroll
         for (int i = 0; i < TC; ++i) db[i] = 0u;
-        if constexpr (FLOOR) {
-            if (!role_b) {
+#pragma unroll
+        for (int w = 0; w < WH; ++w) S[w] = 0u;
+        // FLOOR: a chunk's decisions packed into one register (bit i = step
+        // t0 + i), so the words die as soon as they arrive
+        auto pack = [&](const uint32_t (&w)[TC]) {
+            uint32_t m = 0u;
+#pragma unroll
+            for (int i = 0; i < TC; ++i) m |= ((w[i] >> (L.s & 31u)) & 1u) << i;
+            return L.active ? m : 0u;
+        };
+        uint32_t dm = 0u;
+        // FLOOR: decision words, issued before the state words so that the
+        // chain waits only for them and word 0
+        auto load_db = [&]() {
+            if constexpr (FLOOR) {
 #pragma unroll
                 for (int i = 0; i < TC; ++i)
                     if ((uint32_t)i < T) db[i] = dword_of(a, (uint32_t)i, L.active ? L.s : 0u);
             }
-        }
+        };
+
+        if constexpr (SPLIT) {
+            // (a1, a2) Two lanes per session: the A wavefronts bring in only
+            // what the word-0 chain reads -- the chain section of the image
+            // (word-0 masks, CDF thresholds, guide table), the outcome and
+            // word 0 -- and start the chain after the first barrier; their
+            // other words arrive during the chain.  The B wavefronts, idle
+            // until the chunk's control is published, stage the mask rows and
+            // tool pairs with direct-to-LDS loads; the chunk barrier (whose
+            // fence waits for those loads) precedes every read of the rows.
+            // The first barrier is a bare s_barrier so that the B loads stay
+            // in flight across it.
+            typedef __attribute__((address_space(3))) void lds_void;
+            const uint32_t c4 = a.chain_words / 4u;
+            if (!role_b) {
+                for (uint32_t blk = wa; blk * 64u < c4; blk += NWAVE) {
+                    const uint32_t j = blk * 64u + lane;
+                    if (j < c4)
+                        __builtin_amdgcn_global_load_lds((const void*)(src + j), (lds_void*)(lds4 + blk * 64u),
+                                                         16, 0, 0);
+                }
+                o = ld32(a.outcome, loff);
+                load_db();
+                s0 = ld32(a.state, loff);
+                __builtin_amdgcn_s_waitcnt(0);  // chain section in LDS, outcome and word 0 in VGPRs
+                if constexpr (FLOOR) dm = pack(db);
+            } else {
+                for (uint32_t blk = wa; c4 + blk * 64u < n4; blk += NWAVE) {
+                    const uint32_t j = c4 + blk * 64u + lane;
+                    if (j < n4)
+                        __builtin_amdgcn_global_load_lds((const void*)(src + j),
+                                                         (lds_void*)(lds4 + c4 + blk * 64u), 16, 0, 0);
+                }
+            }
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            // every lane's words in one place (so that both roles keep them
+            // in the same registers and no copy waits for them); the A lanes
+            // read word 0 a second time
 #pragma unroll
-        for (int w = 0; w < WH; ++w)
-            S[w] = (EXACT || wbase + (uint32_t)w < W) ? ld32(a.state + (size_t)(wbase + w) * ldw, loff) : 0u;
-        // Blocks past the image end repeat its last block (same value, same
-        // address), so the writes need no branch either.
+            for (int w = 0; w < WH; ++w)
+                if (EXACT || wbase + (uint32_t)w < W) S[w] = ld32(a.state + (size_t)(wbase + w) * ldw, loff);
+        } else {
+            // (a1, a2) One lane per session: the first batch of the image,
+            // then the outcome and the state words.  Vector-memory loads
+            // complete in order, so the image batch can be written to LDS
+            // while the state loads are still in flight.
+            u32x4* dst = reinterpret_cast<u32x4*>(lds4);
+            u32x4 v[SB];
 #pragma unroll
-        for (int k = 0; k < SB; ++k) {
-            const uint32_t j = tid + (uint32_t)k * WG;
-            dst[j < n4 ? j : n4 - 1u] = v[k];
+            for (int k = 0; k < SB; ++k) {
+                const uint32_t j = tid + (uint32_t)k * WG;
+                v[k] = src[j < n4 ? j : n4 - 1u];
+            }
+            o = ld32(a.outcome, loff);
+            load_db();
+#pragma unroll
+            for (int w = 0; w < WH; ++w)
+                if (EXACT || (uint32_t)w < W) S[w] = ld32(a.state + (size_t)w * ldw, loff);
+            // Blocks past the image end repeat its last block (same value,
+            // same address), so the writes need no branch either.
+#pragma unroll
+            for (int k = 0; k < SB; ++k) {
+                const uint32_t j = tid + (uint32_t)k * WG;
+                dst[j < n4 ? j : n4 - 1u] = v[k];
+            }
+            for (uint32_t j = tid + (uint32_t)SB * WG; j < n4; j += WG) dst[j] = src[j];
+            __syncthreads();
+            if constexpr (FLOOR) dm = pack(db);
+            s0 = S[0];
         }
-        for (uint32_t j = tid + (uint32_t)SB * WG; j < n4; j += WG) dst[j] = src[j];
-        __syncthreads();
 
         // per-wavefront constants of the compaction
         const uint32_t in_c = L.s - L.b;
@@ -832,39 +905,35 @@ struct ChainF {
             }
         }
 
-        // FLOOR: this chunk's decisions packed into one register (bit i =
-        // step t0 + i), so the words die as soon as they arrive
-        auto pack = [&](const uint32_t (&w)[TC]) {
-            uint32_t m = 0u;
-#pragma unroll
-            for (int i = 0; i < TC; ++i) m |= ((w[i] >> (L.s & 31u)) & 1u) << i;
-            return L.active ? m : 0u;
-        };
-        uint32_t dm = 0u;
-        if constexpr (FLOOR) dm = pack(db);
-
-        uint32_t s0 = S[0];  // word 0 of the chain (A lanes)
         uint32_t step = a.step0;
         uint32_t* p_sid = a.eff_sid;
         uint32_t* p_tool = a.eff_tool;
         uint32_t* p_pay = a.eff_payload;
         uint32_t* p_cnt = a.n_taken;
 
-        for (uint32_t t0 = 0; t0 < T; t0 += TC) {
+        // The chain of the chunk starting at step t0 (A lanes): records its
+        // control and addends, then publishes the counts and (SPLIT) the
+        // control.  Chunk 0's chain runs ahead of the chunk loop, so that no
+        // wait for the state words still in flight is placed before it.
+        uint32_t ctl[TC], add[TC];
+        auto chain_chunk = [&](uint32_t t0) {
             const uint32_t n = (T - t0) < (uint32_t)TC ? (T - t0) : (uint32_t)TC;
-            uint32_t ctl[TC], add[TC];
 #pragma unroll
             for (int i = 0; i < TC; ++i) {
                 ctl[i] = 0u;
                 add[i] = 0u;
             }
-
             if (!role_b) {
+                // The chain is a serial dependence through two hashes per
+                // step; raised issue priority keeps it moving while other
+                // wavefronts of the SIMD replay (throughput work that fills
+                // the gaps).
+                __builtin_amdgcn_s_setprio(3);
                 if constexpr (FLOOR)
                     if (t0 != 0u) dm = pack(db);
                 // chain: word 0 only
                 uint32_t r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
-                uint32_t m0 = lds[__umul24(r, RS) >> 2];  // taken mask of word 0, row r
+                uint32_t m0 = lds[r];  // taken mask of word 0 on route r (chain section)
 #pragma unroll
                 for (int i = 0; i < TC; ++i) {
                     if ((uint32_t)i >= n) continue;
@@ -880,7 +949,7 @@ struct ChainF {
                     s0 = (rotr32(s0, dk ? 0u : sh) ^ (dk ? m0 : 0u)) + oo;
                     o = dev_fmix32(s0);
                     r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
-                    m0 = lds[__umul24(r, RS) >> 2];
+                    m0 = lds[r];
                     step += 1u;
                 }
                 // FLOOR: the next chunk's decision words, in flight during
@@ -907,7 +976,13 @@ struct ChainF {
                         lds_x[(2 * i + 1) * (NWAVE * 64) + alane] = add[i];
                     }
                 }
+                __builtin_amdgcn_s_setprio(0);
             }
+        };
+
+        chain_chunk(0u);
+        for (uint32_t t0 = 0; t0 < T; t0 += TC) {
+            const uint32_t n = (T - t0) < (uint32_t)TC ? (T - t0) : (uint32_t)TC;
             if constexpr (MULTI || SPLIT) __syncthreads();
             if (role_b) {
 #pragma unroll
@@ -932,7 +1007,7 @@ struct ChainF {
                 const uint32_t c = ctl[0];
                 const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
 #pragma unroll
-                for (int q = 0; q < NBH; ++q) mc[q] = lds128(lds, rowoff + 16u * q);
+                for (int q = 0; q < NBH; ++q) mc[q] = lds128(lds_rows, rowoff + 16u * q);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[k] : 0u;
                 tpc = lds_tools[c >> 6];
@@ -945,7 +1020,7 @@ struct ChainF {
                     const uint32_t c = ctl[i + 1];
                     const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
 #pragma unroll
-                    for (int q = 0; q < NBH; ++q) mn[q] = lds128(lds, rowoff + 16u * q);
+                    for (int q = 0; q < NBH; ++q) mn[q] = lds128(lds_rows, rowoff + 16u * q);
 #pragma unroll
                     for (int k = 0; k < 4; ++k) cn[k] = MULTI ? cq0[(i + 1) * CNT_STRIDE + k] : 0u;
                     tpn = lds_tools[c >> 6];
@@ -1005,8 +1080,10 @@ struct ChainF {
             }
             // the counts and the control buffer are rewritten by the next
             // chunk only after every wavefront has finished reading them
-            if constexpr (MULTI || SPLIT)
-                if (t0 + TC < T) __syncthreads();
+            if (t0 + TC < T) {
+                if constexpr (MULTI || SPLIT) __syncthreads();
+                chain_chunk(t0 + TC);
+            }
         }
 
         // (a9) store the state and (A lanes) the next outcome (the row
@@ -1268,7 +1345,7 @@ struct rc_cohort {
     bool full = true;
     int route_kind = 0;  // RK_POW2 / RK_MOD / RK_CDF
     uint32_t nwave = 4;
-    uint32_t img_words = 0, tools_off = 0, cdf_off = 0, guide_off = 0;
+    uint32_t img_words = 0, tools_off = 0, cdf_off = 0, guide_off = 0, rows_off = 0, chain_words = 0;
     size_t chain_lds_bytes = 0;
     uint32_t chain_threads = 256;  // threads of a chain workgroup
     std::vector<uint32_t> offsets;  // host copy [C+1]
@@ -1527,6 +1604,8 @@ int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
     a.tools_off = h->tools_off;
     a.cdf_off = h->cdf_off;
     a.guide_off = h->guide_off;
+    a.rows_off = h->rows_off;
+    a.chain_words = h->chain_words;
     a.dbits = dbits;
     a.dwords = (b->ld + 31u) / 32u;
     const uint32_t grid = a.bins_a_n + a.bins_b_n;  // one workgroup per bin
@@ -1675,22 +1754,31 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     // table image layout (see the file comment)
     const size_t full_bytes = (size_t)(R + 1u) * (h->wmax + 4u) * 4u;
     h->full = h->wmax <= 16u || full_bytes <= FULL_IMAGE_LIMIT;
+    // Full image: [word-0 masks | CDF thresholds | guide] (the chain
+    // section, everything the word-0 chain reads), then the mask rows, then
+    // the tool pairs.  Table image: the raw rows, then thresholds and guide.
     const uint32_t row_words = h->full ? h->wmax : 16u;
     const uint32_t tab_words = (R + 1u) * (h->full ? row_words + 4u : row_words);
-    h->tools_off = tab_words;
-    h->cdf_off = h->tools_off + (h->full ? ((R + 3u) & ~3u) : 0u);
-    h->guide_off = h->cdf_off + ((h->ra.cdf_n + 3u) & ~3u);
+    auto pad4 = [](uint32_t x) { return (x + 3u) & ~3u; };
+    const uint32_t m0_words = h->full ? pad4(R + 1u) : 0u;
+    h->cdf_off = h->full ? m0_words : tab_words;
+    h->guide_off = h->cdf_off + pad4(h->ra.cdf_n);
+    const uint32_t after_guide = h->full ? tab_words + pad4(R) : 0u;  // rows and tools
     uint32_t guide_bits = 0, guide_n = 0;
     if (h->ra.mode == RC_ROUTE_CDF) {
         const uint32_t gmin = ceil_log2(R) < 1u ? 1u : ceil_log2(R);
         guide_bits = gmin + 2u < 12u ? gmin + 2u : (gmin > 12u ? gmin : 12u);
         while (guide_bits > gmin &&
-               ((size_t)h->guide_off + (((1u << guide_bits) + 1u + 3u) & ~3u)) * 4u + 256u > LDS_TWO_PER_CU)
+               ((size_t)h->guide_off + pad4((1u << guide_bits) + 1u) + after_guide) * 4u + 256u > LDS_TWO_PER_CU)
             --guide_bits;
         guide_n = (1u << guide_bits) + 1u;
         h->ra.guide_shift = 32u - guide_bits;
     }
-    h->img_words = h->guide_off + ((guide_n + 3u) & ~3u);
+    const uint32_t guide_end = h->guide_off + pad4(guide_n);
+    h->chain_words = h->full ? guide_end : 0u;
+    h->rows_off = h->full ? guide_end : 0u;
+    h->tools_off = h->rows_off + tab_words;
+    h->img_words = h->full ? h->tools_off + pad4(R) : guide_end;
     const size_t lds_image = (size_t)h->img_words * 4u;
     h->nwave = h->full ? 4u : 8u;
     // image, then the count exchange ([16][nwave + 4] words; the table chain
@@ -1733,6 +1821,8 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
         ia.guide_n = guide_n;
         ia.guide_shift = h->ra.guide_shift;
         ia.total_words = h->img_words;
+        ia.m0_words = m0_words;
+        ia.rows_off = h->rows_off;
         hipLaunchKernelGGL(rc_prep_kernel, dim3((h->img_words + 255u) / 256u), dim3(256), 0, 0, ia);
         uint32_t span = 0;
         if (launch_ok() != RC_OK || hipMemcpy(&span, h->d_span, 4, hipMemcpyDeviceToHost) != hipSuccess)
