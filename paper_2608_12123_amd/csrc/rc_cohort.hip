@@ -120,6 +120,13 @@ __device__ __forceinline__ uint32_t mul_small(uint32_t t) {
     else return opaque((mul_small<7>(t) << 1) + t);  // 15
 }
 
+// (t << 4) + m in one instruction.
+__device__ __forceinline__ uint32_t lshl4_add(uint32_t t, uint32_t m) {
+    uint32_t r;
+    asm("v_lshl_add_u32 %0, %1, 4, %2" : "=v"(r) : "v"(t), "v"(m));
+    return r;
+}
+
 // A uniform value (kept in an SGPR) whose provenance is hidden.  Volatile,
 // so that address arithmetic derived from it is not hoisted out of the loop
 // it sits in, nor shared between two places that recompute it.
@@ -218,7 +225,9 @@ __device__ __forceinline__ uint32_t route_of(uint32_t o, const RouteArgs& ra,
             const uint32_t i = pos + stp;
             const uint32_t j = i < hi ? i : hi;          // min(i, hi)
             const uint32_t v = cdf[(j > 1u ? j : 1u) - 1u];  // always in range
-            pos = (i <= hi && v <= o) ? i : pos;
+            // both tests evaluated (no short circuit), so the read needs no
+            // branch around it
+            pos = ((i <= hi) & (v <= o)) ? i : pos;
         }
         return pos;
     }
@@ -494,7 +503,9 @@ __device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[1
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
         constexpr int base = 16 * B;
-        M[j] = after_word((tv[j] << 4) + M[j], S[base + j - 16]);
+        // one v_lshl_add_u32 per mask (written out, so that the shift is
+        // not computed once and kept for every band)
+        M[j] = after_word(lshl4_add(tv[j], M[j]), S[base + j - 16]);
         if (EXACT || (uint32_t)(base + j) < W) S[base + j] = (rotr32(S[base + j], sh) ^ M[j]) + oo;
     }
 }
