@@ -328,6 +328,95 @@ def cpu_baseline(inp, T, min_seconds):
                          os.cpu_count() or 0)}, first
 
 
+def oracle_call_times(orc, inp, T, seconds):
+    """Seconds per call of the oracle's C entry point on preallocated buffers
+    (one direct ctypes call per sample, no Python-side copies)."""
+    import ctypes
+    p32 = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+    state, outcome = inp.state.copy(), inp.outcome.copy()
+    ld = state.shape[1]
+    sid = np.zeros((T, ld), dtype=np.uint32)
+    tool = np.zeros((T, ld), dtype=np.uint32)
+    pay = np.zeros((T, ld, 4), dtype=np.uint32)
+    cnt = np.zeros((T, inp.n_cohorts), dtype=np.uint32)
+    off, tab = np.ascontiguousarray(inp.cohort_offsets), np.ascontiguousarray(inp.table).reshape(-1)
+    cdf = None if inp.route_cdf is None else np.ascontiguousarray(inp.route_cdf)
+    args = (inp.n_sessions, inp.n_words, inp.n_routes, inp.n_cohorts, p32(off), p32(tab),
+            inp.route_mode, None if cdf is None else p32(cdf), inp.decide_thr, p32(state),
+            p32(outcome), p32(sid), p32(tool), p32(pay), p32(cnt), ld, 0, T, 0, inp.n_cohorts, None)
+    fn = orc.lib.rc_oracle_run_chain
+    out = []
+    t_end = time.perf_counter() + seconds
+    while len(out) < 5 or time.perf_counter() < t_end:
+        t0 = time.perf_counter()
+        fn(*args)
+        out.append(time.perf_counter() - t0)
+    return out
+
+
+KR_SIZES = (32, 64, 128, 256, 512, 1024, 2048, 4096)
+KR_STEPS = (1, 2, 4, 8, 16, 32)
+
+
+def safe_suffix_threshold(rc, wk, sizes=KR_SIZES, steps=KR_STEPS, gpu_reps=200, cpu_seconds=0.05):
+    """The hardware threshold K_r of the paper's model (Section 3, "Events and
+    the hardware threshold"): the start of a measured safe suffix -- the
+    smallest tested batch size from which every larger tested size is faster
+    on the device-resident chain than on the named baseline, here the
+    single-threaded oracle on the host cores.
+
+    A batch of K sessions is one invocation over cohorts of min(K, 256)
+    sessions (W = 32, R = 64 Zipf(1.1) routes, p = 0.3: the K = 256
+    workload's shape), chained T steps.  GPU: median microseconds of one
+    synchronized invocation (launch, run, stream sync: the latency an online
+    caller sees).  CPU: median microseconds of the oracle on the same inputs.
+    K_r is null when even the largest tested size is not faster."""
+    import torch
+    import oracle
+    orc = oracle.load()
+    stream = torch.cuda.current_stream().cuda_stream
+    rows = []
+    for K in sizes:
+        cs = min(K, 256)
+        inp = wk.make_custom(n_words=32, n_routes=64, route_mode=wk.ROUTE_CDF, decide_thr=19661,
+                             cohort_sizes=[cs] * (K // cs), n_steps=max(steps), seed_key=7000 + K)
+        h = rc.rc_cohort_create(n_sessions=inp.n_sessions, n_words=32, n_routes=64,
+                                cohort_offsets=inp.cohort_offsets, table=inp.table,
+                                route_mode=inp.route_mode, route_cdf=inp.route_cdf,
+                                decide_thr=inp.decide_thr)
+        try:
+            sets = Sets(rc, inp, max(steps), 1)
+            for T in steps:
+                for _ in range(10):
+                    rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_RESIDENT, 0, inp.n_cohorts, stream)
+                torch.cuda.synchronize()
+                g = []
+                for _ in range(gpu_reps):
+                    t0 = time.perf_counter()
+                    rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_RESIDENT, 0, inp.n_cohorts, stream)
+                    torch.cuda.current_stream().synchronize()
+                    g.append(time.perf_counter() - t0)
+                c = oracle_call_times(orc, inp, T, cpu_seconds)
+                rows.append({"K": K, "T": T, "gpu_us": round(float(np.median(g)) * 1e6, 2),
+                             "cpu_us": round(float(np.median(c)) * 1e6, 2)})
+        finally:
+            rc.rc_cohort_destroy(h)
+    k_r = {}
+    for T in steps:
+        r = sorted((x for x in rows if x["T"] == T), key=lambda x: x["K"])
+        kr = None
+        for x in reversed(r):
+            if x["gpu_us"] < x["cpu_us"]:
+                kr = x["K"]
+            else:
+                break
+        k_r[str(T)] = kr
+    return {"k_r_by_T": k_r, "rows": rows,
+            "note": "smallest tested K from which every larger tested K is faster on the resident "
+                    "chain (synchronized invocation) than on the single-threaded oracle; cohorts "
+                    "of min(K, 256) sessions, W=32, R=64 Zipf(1.1), p=0.3"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -339,6 +428,7 @@ def main():
     ap.add_argument("--no-mechanisms", action="store_true", help="skip the five-workload table")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kr", action="store_true", help="skip the safe-suffix K_r sweep")
     ap.add_argument("--profile-only", action="store_true",
                     help="only the resident timed loop (for rocprofv3 counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -458,6 +548,8 @@ def main():
                     "bitmap with no predicate (a structural floor, not an online policy)",
         }
         if cpu is not None:
+            if not args.no_kr:
+                cpu["safe_suffix_k_r"] = safe_suffix_threshold(rc, wk)
             out["cpu_baseline"] = cpu
         out["hbm_measured"] = hbm_measured()
         if not args.no_mechanisms:
