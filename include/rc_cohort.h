@@ -228,6 +228,50 @@ int rc_plan_lanes(const rc_cohort_desc *desc, uint32_t lanes_per_workgroup,
                   uint32_t *lane_session, uint32_t *lane_cohort, uint32_t capacity,
                   uint32_t *n_lanes);
 
+/*
+ * Cohort shares of a set of control events (host only; no device is used).
+ * The paper's model (Section 3 "Events and the hardware threshold" and "Four
+ * shares"): event i has an integer-nanosecond release t_i, a latest launch
+ * t_i + delta (the equal relative deadlines of Section 4) and a route r_i; a
+ * batch is feasible when its events share a route, number at least K_r, and
+ * admit a launch time inside every member's [t_i, t_i + delta]
+ * (Eq. feasible-batch; comparisons inclusive).  Returned numerators (divide
+ * by n_events for the shares):
+ *   fixed_eligible    F:  events in buckets (origin-aligned half-open window
+ *                     [origin + k delta, origin + (k+1) delta), route) of at
+ *                     least K_r events (Eq. fixed);
+ *   packed            P*: the largest number of events covered by disjoint
+ *                     feasible batches (Eq. dp, Algorithm 1: grouped sort,
+ *                     moving left pointer, monotone deque), exact;
+ *   overlap_eligible  U:  events whose route's active count reaches K_r at
+ *                     some launch time inside their own interval (Eq. upper);
+ *   n_batches         batches of the returned witness schedule.
+ * F <= P* <= U always (Proposition "Boundary ordering").
+ *   release_ns, route  HOST arrays of n_events; route[i] < n_routes.
+ *   k_of_route         HOST array of n_routes thresholds, each >= 1.
+ *   delta_ns           >= 1; |release|, delta at most INT64_MAX / 4.
+ *   batch_of_event     optional HOST array of n_events (NULL: not written):
+ *                      the witness, the batch of every event or 0xFFFFFFFF
+ *                      for events left out; batches are numbered by route,
+ *                      then by first release, and each is a contiguous run
+ *                      of the route's release order (Section 4, "Contiguous
+ *                      block form").
+ * Errors: RC_E_INVALID for a NULL required pointer, a route out of range, a
+ * zero threshold, delta < 1 or n_events >= 2^32 - 1 (nothing written);
+ * RC_E_NOMEM when host memory runs out.
+ */
+typedef struct {
+    uint64_t n_events;
+    uint64_t fixed_eligible;   /* numerator of F  */
+    uint64_t packed;           /* numerator of P* */
+    uint64_t overlap_eligible; /* numerator of U  */
+    uint64_t n_batches;
+} rc_pack_result;
+
+int rc_pack_shares(const int64_t *release_ns, const uint32_t *route, uint64_t n_events,
+                   const uint32_t *k_of_route, uint32_t n_routes, int64_t delta_ns,
+                   int64_t window_origin_ns, uint32_t *batch_of_event, rc_pack_result *out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -27,7 +27,7 @@ RC_MODE_RESIDENT, RC_MODE_HOST_ROUNDTRIP = 0, 1
 EXPORTED = [
     "rc_cohort_create", "rc_cohort_step", "rc_cohort_run_chain", "rc_cohort_run_floor",
     "rc_cohort_destroy", "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info",
-    "rc_plan_lanes",
+    "rc_plan_lanes", "rc_pack_shares",
 ]
 
 _P32 = ctypes.POINTER(ctypes.c_uint32)
@@ -56,6 +56,16 @@ class RcBuffers(ctypes.Structure):
         ("eff_payload", ctypes.c_void_p),
         ("n_taken", ctypes.c_void_p),
         ("ld", ctypes.c_uint32),
+    ]
+
+
+class RcPackResult(ctypes.Structure):
+    _fields_ = [
+        ("n_events", ctypes.c_uint64),
+        ("fixed_eligible", ctypes.c_uint64),
+        ("packed", ctypes.c_uint64),
+        ("overlap_eligible", ctypes.c_uint64),
+        ("n_batches", ctypes.c_uint64),
     ]
 
 
@@ -103,6 +113,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rc_plan_lanes.argtypes = [ctypes.POINTER(RcCohortDesc), ctypes.c_uint32, _P32, _P32,
                                   ctypes.c_uint32, _P32]
     lib.rc_plan_lanes.restype = ctypes.c_int
+    lib.rc_pack_shares.argtypes = [ctypes.POINTER(ctypes.c_int64), _P32, ctypes.c_uint64, _P32,
+                                   ctypes.c_uint32, ctypes.c_int64, ctypes.c_int64, _P32,
+                                   ctypes.POINTER(RcPackResult)]
+    lib.rc_pack_shares.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -216,6 +230,31 @@ def rc_plan_lanes(*, cohort_offsets, n_words=4, n_routes=1, lanes_per_workgroup=
     _check(lib.rc_plan_lanes(ctypes.byref(desc), lanes_per_workgroup, _ptr(ses), _ptr(coh),
                              n.value, ctypes.byref(n)), "rc_plan_lanes")
     return ses, coh
+
+
+def rc_pack_shares(*, release_ns, route, k_of_route, delta_ns: int, window_origin_ns: int = 0,
+                   witness: bool = False, check: bool = True):
+    """Cohort shares (numerators of F, P*, U) of a set of events; with
+    ``witness``, also the batch of every event (0xFFFFFFFF: left out).
+    Host computation in the library (no device)."""
+    t = np.ascontiguousarray(release_ns, dtype=np.int64)
+    r = _u32(route)
+    k = _u32(k_of_route)
+    n = t.size
+    assert r.size == n
+    bat = np.empty(n, dtype=np.uint32) if witness else None
+    res = RcPackResult()
+    st = load_library().rc_pack_shares(
+        t.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)) if n else None, _ptr(r) if n else None,
+        n, _ptr(k), k.size, int(delta_ns), int(window_origin_ns),
+        _ptr(bat) if witness and n else None, ctypes.byref(res))
+    if check:
+        _check(st, "rc_pack_shares")
+    if st != RC_OK:
+        return st
+    out = {"n_events": res.n_events, "fixed_eligible": res.fixed_eligible, "packed": res.packed,
+           "overlap_eligible": res.overlap_eligible, "n_batches": res.n_batches}
+    return (out, bat) if witness else out
 
 
 # ---------------------------------------------------------------------------

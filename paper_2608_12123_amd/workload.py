@@ -285,9 +285,7 @@ def make_inputs(wl: Workload, chunk: int = 0, ld: Optional[int] = None,
         outcome0 = uniform_u32(N, wl.cid, chunk, A_OUTCOME, root=root)
     else:
         N = wl.n_sessions
-        times = poisson_arrivals_ns(N, ARRIVAL_RATE_PER_S, wl.cid, chunk, A_ARRIVAL)
-        arr_out = uniform_u32(N, wl.cid, chunk, A_ARRIVAL_OUTCOME, root=root)
-        routes = route_of_outcomes_cdf(arr_out, cdf) if cdf is not None else arr_out % R
+        times, routes, arr_out = arrival_events(wl, chunk, root=root)
         order, info = form_cohorts(times, routes, DEADLINE_NS)
         outcome0 = arr_out[order]
         offsets = np.concatenate([[0], np.cumsum(info["sizes_array"])]).astype(np.uint32)
@@ -303,6 +301,21 @@ def make_inputs(wl: Workload, chunk: int = 0, ld: Optional[int] = None,
         outcome[N:] = 0x5A5A5A5A
     return Inputs(wl, chunk, N, W, R, wl.route_mode, wl.decide_thr, wl.n_steps,
                   offsets, table, cdf, state, outcome, stats)
+
+
+def arrival_events(wl: Workload, chunk: int = 0, root: int = ROOT_SEED):
+    """The control events of a variable-cohort workload: integer-ns Poisson
+    releases, the route of each arrival (of its outcome, by the workload's
+    route rule) and the arrival outcomes.  Returns (times, routes, outcomes)."""
+    assert not wl.cohort_size, "uniform workloads have no arrival stream"
+    N, R = wl.n_sessions, wl.n_routes
+    times = poisson_arrivals_ns(N, ARRIVAL_RATE_PER_S, wl.cid, chunk, A_ARRIVAL)
+    arr_out = uniform_u32(N, wl.cid, chunk, A_ARRIVAL_OUTCOME, root=root)
+    if wl.route_mode == ROUTE_CDF:
+        routes = route_of_outcomes_cdf(arr_out, zipf_cdf(R, wl.zipf_s))
+    else:
+        routes = arr_out % R
+    return times, routes.astype(np.uint32), arr_out
 
 
 def make_custom(*, n_words: int, n_routes: int, route_mode: int, decide_thr: int,
