@@ -38,7 +38,7 @@ METRIC = ("transitions/sec and µs per chained cohort step (resident vs host rou
           "HBM GB/s")
 HBM_PEAK_GBS = 8000.0
 INFINITY_CACHE_BYTES = 256 << 20
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "rc_chain_kernel_s100k_traffic.txt")
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "rc_chain_kernel_%s_traffic.txt")  # by workload
 KERNEL_SRC = os.path.join(ROOT, "paper_2608_12123_amd", "csrc", "rc_cohort.hip")
 
 
@@ -60,13 +60,14 @@ def kernel_src_hash():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def stored_traffic(steps_hint):
-    """HBM traffic per launch from the committed rocprofv3 counter summary,
-    valid only while the kernel source is unchanged."""
-    if not os.path.exists(PROFILE_TRAFFIC):
+def stored_traffic(workload_key):
+    """HBM traffic per launch of the workload from the committed rocprofv3
+    counter summary, valid only while the kernel source is unchanged."""
+    path = PROFILE_TRAFFIC % workload_key
+    if not os.path.exists(path):
         return None
     vals = {}
-    with open(PROFILE_TRAFFIC) as f:
+    with open(path) as f:
         for line in f:
             if "=" in line and not line.startswith("#"):
                 k, v = line.split("=", 1)
@@ -417,6 +418,35 @@ def safe_suffix_threshold(rc, wk, sizes=KR_SIZES, steps=KR_STEPS, gpu_reps=200, 
                     "of min(K, 256) sessions, W=32, R=64 Zipf(1.1), p=0.3"}
 
 
+def cohort_former(rc, wk, ks=(32, 64, 128, 256), reps=3):
+    """The library's cohort former on the 1M-event Poisson arrival stream of
+    the variable-cohort workload (Zipf routes, delta = the 50 ms launch
+    deadline, one K for every route): the shares F <= P* <= U, the gap
+    closure G = (P* - F) / (U - F), and the host rate of the whole call
+    (grouped sort, Algorithm 1 with witness, U)."""
+    wl = wk.WORKLOADS["s1m"]
+    times, routes, _ = wk.arrival_events(wl)
+    n = times.size
+    rows = {}
+    for K in ks:
+        k = np.full(wl.n_routes, K, dtype=np.uint32)
+        best = float("inf")
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            res, _bat = rc.rc_pack_shares(release_ns=times, route=routes, k_of_route=k,
+                                          delta_ns=wk.DEADLINE_NS, witness=True)
+            best = min(best, time.perf_counter() - t0)
+        f, p, u = (res[x] / n for x in ("fixed_eligible", "packed", "overlap_eligible"))
+        rows["K%d" % K] = {
+            "F": round(f, 5), "P_star": round(p, 5), "U": round(u, 5),
+            "G": round((p - f) / (u - f), 4) if u > f else None,
+            "batches": res["n_batches"], "ms": round(best * 1e3, 2),
+            "events_per_s": round(n / best, 1),
+        }
+    return {"events": n, "routes": wl.n_routes, "delta_ms": wk.DEADLINE_NS / 1e6,
+            "where": "host (library C++ code, one thread)", "by_K": rows}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -429,6 +459,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kr", action="store_true", help="skip the safe-suffix K_r sweep")
+    ap.add_argument("--no-former", action="store_true", help="skip the cohort-former shares")
     ap.add_argument("--profile-only", action="store_true",
                     help="only the resident timed loop (for rocprofv3 counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -493,7 +524,7 @@ def main():
     k_avg_ms = region_ms / args.steps
     abytes = algorithmic_bytes(N, W, T, C)
     achieved = abytes / (k_avg_ms * 1e-3) / 1e9
-    traffic = stored_traffic(args.steps)
+    traffic = stored_traffic(wl.key)
     out = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -552,6 +583,8 @@ def main():
                 cpu["safe_suffix_k_r"] = safe_suffix_threshold(rc, wk)
             out["cpu_baseline"] = cpu
         out["hbm_measured"] = hbm_measured()
+        if not args.no_former:
+            out["cohort_former"] = cohort_former(rc, wk)
         if not args.no_mechanisms:
             out["mechanisms"] = {k: mechanism_row(rc, wk, k) for k in wk.WORKLOAD_ORDER}
     rc.rc_cohort_destroy(h)
