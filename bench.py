@@ -418,32 +418,51 @@ def safe_suffix_threshold(rc, wk, sizes=KR_SIZES, steps=KR_STEPS, gpu_reps=200, 
                     "of min(K, 256) sessions, W=32, R=64 Zipf(1.1), p=0.3"}
 
 
-def cohort_former(rc, wk, ks=(32, 64, 128, 256), reps=3):
-    """The library's cohort former on the 1M-event Poisson arrival stream of
-    the variable-cohort workload (Zipf routes, delta = the 50 ms launch
-    deadline, one K for every route): the shares F <= P* <= U, the gap
-    closure G = (P* - F) / (U - F), and the host rate of the whole call
-    (grouped sort, Algorithm 1 with witness, U)."""
+ONLINE_CAPACITY = 4096  # queue capacity per route of the online compactor
+
+
+def cohort_former(rc, wk, latency_ns, ks=(32, 64, 128, 256), reps=3):
+    """The library's cohort former and online compactor on the 1M-event
+    Poisson arrival stream of the variable-cohort workload (Zipf routes,
+    delta = the 50 ms launch deadline, one K for every route): the shares
+    F <= P* <= U, the gap closure G = (P* - F) / (U - F), the online share A
+    and its recovery R_A = (A - F) / (P* - F), and the host time of each call
+    (former: grouped sort, Algorithm 1 with witness, U; compactor: grouped
+    sort and the policy sweep).  ``latency_ns`` is the launch-to-start
+    latency the compactor budgets before each deadline."""
     wl = wk.WORKLOADS["s1m"]
     times, routes, _ = wk.arrival_events(wl)
     n = times.size
+
+    def best_of(fn):
+        best, out = float("inf"), None
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            out = fn()
+            best = min(best, time.perf_counter() - t0)
+        return best, out
+
     rows = {}
     for K in ks:
         k = np.full(wl.n_routes, K, dtype=np.uint32)
-        best = float("inf")
-        for _ in range(reps):
-            t0 = time.perf_counter()
-            res, _bat = rc.rc_pack_shares(release_ns=times, route=routes, k_of_route=k,
-                                          delta_ns=wk.DEADLINE_NS, witness=True)
-            best = min(best, time.perf_counter() - t0)
+        t_pack, (res, _bat) = best_of(lambda: rc.rc_pack_shares(
+            release_ns=times, route=routes, k_of_route=k, delta_ns=wk.DEADLINE_NS, witness=True))
+        t_on, (on, _b, _l) = best_of(lambda: rc.rc_online_compact(
+            release_ns=times, route=routes, k_of_route=k, delta_ns=wk.DEADLINE_NS,
+            latency_ns=latency_ns, capacity=ONLINE_CAPACITY, witness=True))
         f, p, u = (res[x] / n for x in ("fixed_eligible", "packed", "overlap_eligible"))
+        a = on["accelerated"] / n
         rows["K%d" % K] = {
             "F": round(f, 5), "P_star": round(p, 5), "U": round(u, 5),
             "G": round((p - f) / (u - f), 4) if u > f else None,
-            "batches": res["n_batches"], "ms": round(best * 1e3, 2),
-            "events_per_s": round(n / best, 1),
+            "A": round(a, 5), "R_A": round((a - f) / (p - f), 4) if p > f else None,
+            "batches": res["n_batches"], "online_batches": on["n_batches"],
+            "online_fallback_deadline": on["fallback_deadline"],
+            "former_ms": round(t_pack * 1e3, 2), "compactor_ms": round(t_on * 1e3, 2),
+            "former_events_per_s": round(n / t_pack, 1),
         }
     return {"events": n, "routes": wl.n_routes, "delta_ms": wk.DEADLINE_NS / 1e6,
+            "online_latency_us": latency_ns / 1e3, "online_capacity": ONLINE_CAPACITY,
             "where": "host (library C++ code, one thread)", "by_K": rows}
 
 
@@ -584,7 +603,13 @@ def main():
             out["cpu_baseline"] = cpu
         out["hbm_measured"] = hbm_measured()
         if not args.no_former:
-            out["cohort_former"] = cohort_former(rc, wk)
+            # launch-to-start budget: the measured synchronized invocation of
+            # a 256-session, 16-step batch when the K_r sweep ran, else 25 us
+            lat_us = 25.0
+            kr = (cpu or {}).get("safe_suffix_k_r")
+            if kr:
+                lat_us = max(r["gpu_us"] for r in kr["rows"] if r["K"] == 256 and r["T"] == 16)
+            out["cohort_former"] = cohort_former(rc, wk, int(round(lat_us * 1e3)))
         if not args.no_mechanisms:
             out["mechanisms"] = {k: mechanism_row(rc, wk, k) for k in wk.WORKLOAD_ORDER}
     rc.rc_cohort_destroy(h)

@@ -249,7 +249,8 @@ int rc_plan_lanes(const rc_cohort_desc *desc, uint32_t lanes_per_workgroup,
  * F <= P* <= U always (Proposition "Boundary ordering").
  *   release_ns, route  HOST arrays of n_events; route[i] < n_routes.
  *   k_of_route         HOST array of n_routes thresholds, each >= 1.
- *   delta_ns           >= 1; |release|, delta at most INT64_MAX / 4.
+ *   delta_ns           >= 1; |release|, delta, |window_origin_ns| at most
+ *                      INT64_MAX / 4.
  *   batch_of_event     optional HOST array of n_events (NULL: not written):
  *                      the witness, the batch of every event or 0xFFFFFFFF
  *                      for events left out; batches are numbered by route,
@@ -257,8 +258,9 @@ int rc_plan_lanes(const rc_cohort_desc *desc, uint32_t lanes_per_workgroup,
  *                      of the route's release order (Section 4, "Contiguous
  *                      block form").
  * Errors: RC_E_INVALID for a NULL required pointer, a route out of range, a
- * zero threshold, delta < 1 or n_events >= 2^32 - 1 (nothing written);
- * RC_E_NOMEM when host memory runs out.
+ * zero threshold, delta < 1, a clock value out of range or
+ * n_events >= 2^32 - 1 (nothing written); RC_E_NOMEM when host memory runs
+ * out.
  */
 typedef struct {
     uint64_t n_events;
@@ -271,6 +273,70 @@ typedef struct {
 int rc_pack_shares(const int64_t *release_ns, const uint32_t *route, uint64_t n_events,
                    const uint32_t *k_of_route, uint32_t n_routes, int64_t delta_ns,
                    int64_t window_origin_ns, uint32_t *batch_of_event, rc_pack_result *out);
+
+/*
+ * Online route compactor (host only): the runtime of Section 9 ("The next
+ * systems test") under one frozen policy, and its achieved share A (the
+ * share of events it accelerates; R_A = (A - F) / (P* - F), Eq.
+ * online-recovery).  Events (same arguments and limits as rc_pack_shares)
+ * arrive in release order into a FIFO queue of their route.  A launch at
+ * host time tau starts on the device at tau + latency_ns, which must be no
+ * later than every member's deadline t_i + delta_ns.  The policy:
+ *   - a queue's trigger is t_oldest + delta - latency; arrivals at or before
+ *     it are queued first;
+ *   - at the trigger, a queue of at least K_r events is launched whole; a
+ *     shorter one sends its oldest event to the CPU (fallback_deadline);
+ *   - a queue that reaches `capacity` events (>= K_r) is launched at the
+ *     arrival that filled it (launched_at_capacity); with capacity < K_r an
+ *     arrival that finds its queue full goes to the CPU (fallback_capacity).
+ * Every launched batch is feasible in the sense of Eq. feasible-batch, so
+ * accelerated <= packed of rc_pack_shares on the same events.
+ *   latency_ns      0 <= latency_ns <= delta_ns.
+ *   capacity        queue capacity per route, >= 1 (0xFFFFFFFF: unlimited).
+ *   batch_of_event  optional HOST array of n_events: the launched batch of
+ *                   every event, 0xFFFFFFFF for the CPU; batches numbered by
+ *                   route, then launch order.
+ *   launch_ns       optional HOST array with room for n_events entries: the
+ *                   launch time of every batch (first n_batches written).
+ * Errors: as rc_pack_shares, and RC_E_INVALID for capacity 0 or a latency
+ * outside [0, delta_ns].
+ */
+typedef struct {
+    uint64_t n_events;
+    uint64_t accelerated;          /* numerator of A */
+    uint64_t fallback_deadline;
+    uint64_t fallback_capacity;
+    uint64_t n_batches;
+    uint64_t launched_at_capacity; /* batches launched because their queue was full */
+} rc_online_result;
+
+int rc_online_compact(const int64_t *release_ns, const uint32_t *route, uint64_t n_events,
+                      const uint32_t *k_of_route, uint32_t n_routes, int64_t delta_ns,
+                      int64_t latency_ns, uint32_t capacity, uint32_t *batch_of_event,
+                      int64_t *launch_ns, rc_online_result *out);
+
+/*
+ * Cohorts of the transition from a batch assignment (host only), so that the
+ * batches of rc_pack_shares or rc_online_compact can be fed to
+ * rc_cohort_create / rc_cohort_run_chain.  Each batch of n events is cut into
+ * ceil(n / max_cohort) cohorts of near-equal size (the first n mod pieces
+ * one larger), its events in index order; events with batch 0xFFFFFFFF are
+ * left out.
+ *   batch_of_event  HOST array of n_events; entries < n_batches or 0xFFFFFFFF.
+ *   max_cohort      >= 1 (the transition takes cohorts of at most 256).
+ *   order           HOST array with room for n_events: the event index of
+ *                   every session, sessions grouped by cohort, cohorts by
+ *                   batch.
+ *   offsets         HOST array with room for n_events + 1: cohort c holds
+ *                   sessions [offsets[c], offsets[c + 1]); offsets[0] = 0.
+ *   n_cohorts       out: the number of cohorts.
+ * Errors: RC_E_INVALID for a NULL pointer, max_cohort 0, n_batches >
+ * n_events, a batch id out of range or n_events >= 2^32 - 1 (nothing
+ * written); RC_E_NOMEM when host memory runs out.
+ */
+int rc_cohorts_from_batches(const uint32_t *batch_of_event, uint64_t n_events, uint64_t n_batches,
+                            uint32_t max_cohort, uint32_t *order, uint32_t *offsets,
+                            uint64_t *n_cohorts);
 
 #ifdef __cplusplus
 }

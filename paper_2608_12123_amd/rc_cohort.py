@@ -27,7 +27,7 @@ RC_MODE_RESIDENT, RC_MODE_HOST_ROUNDTRIP = 0, 1
 EXPORTED = [
     "rc_cohort_create", "rc_cohort_step", "rc_cohort_run_chain", "rc_cohort_run_floor",
     "rc_cohort_destroy", "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info",
-    "rc_plan_lanes", "rc_pack_shares",
+    "rc_plan_lanes", "rc_pack_shares", "rc_online_compact", "rc_cohorts_from_batches",
 ]
 
 _P32 = ctypes.POINTER(ctypes.c_uint32)
@@ -66,6 +66,17 @@ class RcPackResult(ctypes.Structure):
         ("packed", ctypes.c_uint64),
         ("overlap_eligible", ctypes.c_uint64),
         ("n_batches", ctypes.c_uint64),
+    ]
+
+
+class RcOnlineResult(ctypes.Structure):
+    _fields_ = [
+        ("n_events", ctypes.c_uint64),
+        ("accelerated", ctypes.c_uint64),
+        ("fallback_deadline", ctypes.c_uint64),
+        ("fallback_capacity", ctypes.c_uint64),
+        ("n_batches", ctypes.c_uint64),
+        ("launched_at_capacity", ctypes.c_uint64),
     ]
 
 
@@ -117,6 +128,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                    ctypes.c_uint32, ctypes.c_int64, ctypes.c_int64, _P32,
                                    ctypes.POINTER(RcPackResult)]
     lib.rc_pack_shares.restype = ctypes.c_int
+    lib.rc_online_compact.argtypes = [ctypes.POINTER(ctypes.c_int64), _P32, ctypes.c_uint64, _P32,
+                                      ctypes.c_uint32, ctypes.c_int64, ctypes.c_int64,
+                                      ctypes.c_uint32, _P32, ctypes.POINTER(ctypes.c_int64),
+                                      ctypes.POINTER(RcOnlineResult)]
+    lib.rc_online_compact.restype = ctypes.c_int
+    lib.rc_cohorts_from_batches.argtypes = [_P32, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
+                                            _P32, _P32, ctypes.POINTER(ctypes.c_uint64)]
+    lib.rc_cohorts_from_batches.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -255,6 +274,60 @@ def rc_pack_shares(*, release_ns, route, k_of_route, delta_ns: int, window_origi
     out = {"n_events": res.n_events, "fixed_eligible": res.fixed_eligible, "packed": res.packed,
            "overlap_eligible": res.overlap_eligible, "n_batches": res.n_batches}
     return (out, bat) if witness else out
+
+
+UNLIMITED = 0xFFFFFFFF  # queue capacity without a limit
+
+
+def _p64(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def rc_online_compact(*, release_ns, route, k_of_route, delta_ns: int, latency_ns: int = 0,
+                      capacity: int = UNLIMITED, witness: bool = False, check: bool = True):
+    """The online route compactor's counts (A's numerator and the
+    fallbacks); with ``witness``, also the batch of every event
+    (0xFFFFFFFF: CPU) and every batch's launch time.  Host computation in
+    the library (no device)."""
+    t = np.ascontiguousarray(release_ns, dtype=np.int64)
+    r = _u32(route)
+    k = _u32(k_of_route)
+    n = t.size
+    assert r.size == n
+    bat = np.empty(n, dtype=np.uint32) if witness else None
+    lt = np.empty(max(n, 1), dtype=np.int64) if witness else None
+    res = RcOnlineResult()
+    st = load_library().rc_online_compact(
+        _p64(t) if n else None, _ptr(r) if n else None, n, _ptr(k), k.size, int(delta_ns),
+        int(latency_ns), int(capacity), _ptr(bat) if witness and n else None,
+        _p64(lt) if witness else None, ctypes.byref(res))
+    if check:
+        _check(st, "rc_online_compact")
+    if st != RC_OK:
+        return st
+    out = {f: getattr(res, f) for f, _ in RcOnlineResult._fields_}
+    return (out, bat, lt[:res.n_batches].copy()) if witness else out
+
+
+def rc_cohorts_from_batches(batch_of_event, n_batches: int, max_cohort: int = 256,
+                            check: bool = True):
+    """(order, offsets): sessions grouped by cohort (event indices) and the
+    cohort offsets, each batch cut into near-equal cohorts of at most
+    ``max_cohort``."""
+    b = _u32(batch_of_event)
+    n = b.size
+    order = np.empty(max(n, 1), dtype=np.uint32)
+    offsets = np.empty(n + 1, dtype=np.uint32)
+    nc = ctypes.c_uint64(0)
+    st = load_library().rc_cohorts_from_batches(_ptr(b) if n else None, n, int(n_batches),
+                                                int(max_cohort), _ptr(order), _ptr(offsets),
+                                                ctypes.byref(nc))
+    if check:
+        _check(st, "rc_cohorts_from_batches")
+    if st != RC_OK:
+        return st
+    c = nc.value
+    return order[:offsets[c]].copy(), offsets[:c + 1].copy()
 
 
 # ---------------------------------------------------------------------------
