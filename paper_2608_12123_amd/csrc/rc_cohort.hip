@@ -64,6 +64,7 @@
 #include <string.h>
 
 #include <new>
+#include <type_traits>
 #include <vector>
 
 #include "rc_cohort.h"
@@ -752,6 +753,27 @@ struct Chain {
 // A lone wavefront issues VALU work at about half the rate a SIMD sustains
 // with several, so the second wavefront per session roughly halves the
 // replay.
+// Workgroup barrier for LDS traffic only: each wavefront waits for its own
+// LDS accesses (lgkmcnt 0; vmcnt and expcnt left at their maxima), not for
+// its global loads and stores, which no other wavefront reads -- so state
+// loads stay in flight across it.  (A workgroup release fence would wait for
+// every outstanding global access as well.)
+// Wait until at most N vector-memory accesses of this wavefront are
+// outstanding (lgkmcnt and expcnt unconstrained).  They complete in issue
+// order, so this waits for everything issued before the last N.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N <= 63, "vmcnt is a 6-bit count");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 // Rows of the mask image are W + 4 words apart (one zero block of padding
 // shifts consecutive rows across the LDS banks), so block q of a row is an
 // immediate offset from the row's byte offset.
@@ -763,8 +785,17 @@ struct ChainF {
     // fill each line from several wavefronts.
     static constexpr bool NTE = false;
     static constexpr uint32_t CNT_STRIDE = NWAVE + 4;
-    static constexpr int WH = SPLIT ? WMAX / 2 : WMAX;  // words per lane
-    static constexpr int NBH = WH / 4;                   // 16-byte blocks per lane
+    // Words per lane.  SPLIT: an A lane holds words [0, WA) of its session
+    // and emits the effects; its B lane holds words [WA, WMAX).  At
+    // WMAX = 32 the A lanes hold only the four payload words: once a
+    // wavefront has issued stores, waiting for any earlier load means
+    // waiting for everything on the vector-memory counter, so a lane that
+    // emits effects should have no load left to wait for -- and the 28 words
+    // of the B lanes then arrive while the effects go out.
+    static constexpr int WA = SPLIT ? (WMAX == 32 ? 4 : WMAX / 2) : WMAX;
+    static constexpr int WB = SPLIT ? WMAX - WA : 0;
+    static constexpr int WS = WA > WB ? WA : WB;  // state registers per lane
+    static constexpr int NBA = WA / 4, NBB = WB / 4;  // 16-byte blocks per lane
     static constexpr uint32_t RS = (WMAX + 4) * 4;       // row stride in bytes
     static constexpr int TC = WMAX <= 32 ? 16 : 8;       // steps per chunk
     static constexpr uint32_t WG = (SPLIT ? 2 : 1) * NWAVE * 64;
@@ -782,7 +813,7 @@ struct ChainF {
         const bool role_b = SPLIT && wv >= (uint32_t)NWAVE;  // uniform per wavefront
         const uint32_t wa = role_b ? wv - NWAVE : wv;         // the plan wavefront it serves
         const uint32_t alane = wa * 64u + lane;                // lane index among the A lanes
-        const uint32_t wbase = role_b ? (uint32_t)WH : 0u;    // first word of this lane
+        const uint32_t wbase = role_b ? (uint32_t)WA : 0u;    // first word of this lane
         const uint32_t W = a.n_words;
         const uint32_t R = a.ra.n_routes;
         const uint32_t T = a.n_steps;
@@ -799,7 +830,7 @@ struct ChainF {
         const uint32_t n4 = a.img_words / 4u;
         // Unconditional loads (idle lanes read session 0 and never store), so
         // that no branch splits the in-order load sequence.
-        uint32_t S[WH];
+        uint32_t S[WS];
         const uint32_t loff = L.active ? soff : 0u;
         const uint32_t ldw = opaque_s(a.ld);
         uint32_t o = 0u;
@@ -811,7 +842,7 @@ struct ChainF {
 #pragma unroll
         for (int i = 0; i < TC; ++i) db[i] = 0u;
 #pragma unroll
-        for (int w = 0; w < WH; ++w) S[w] = 0u;
+        for (int w = 0; w < WS; ++w) S[w] = 0u;
         // FLOOR: a chunk's decisions packed into one register (bit i = step
         // t0 + i), so the words die as soon as they arrive
         auto pack = [&](const uint32_t (&w)[TC]) {
@@ -831,53 +862,50 @@ struct ChainF {
             }
         };
 
-        if constexpr (SPLIT) {
-            // (a1, a2) Two lanes per session: the A wavefronts bring in only
-            // what the word-0 chain reads -- the chain section of the image
-            // (word-0 masks, CDF thresholds, guide table), the outcome and
-            // word 0 -- and start the chain after the first barrier; their
-            // other words arrive during the chain.  The B wavefronts, idle
-            // until the chunk's control is published, stage the mask rows and
-            // tool pairs with direct-to-LDS loads; the chunk barrier (whose
-            // fence waits for those loads) precedes every read of the rows.
-            // The first barrier is a bare s_barrier so that the B loads stay
-            // in flight across it.
-            typedef __attribute__((address_space(3))) void lds_void;
+        // (a1, a2) Staging.  SPLIT, A wavefronts: only what the word-0 chain
+        // reads -- the chain section of the image (word-0 masks, CDF
+        // thresholds, guide table), the outcome and word 0 -- so that the
+        // chain starts after the first barrier.  SPLIT, B wavefronts (idle
+        // until the chunk's control is published): the mask rows and tool
+        // pairs, with direct-to-LDS loads that stay in flight across the
+        // first (bare) barrier; every B lane waits for its own before the
+        // barrier that precedes the first read of the rows.
+        typedef __attribute__((address_space(3))) void lds_void;
+        auto stage_a = [&]() {
             const uint32_t c4 = a.chain_words / 4u;
-            if (!role_b) {
-                for (uint32_t blk = wa; blk * 64u < c4; blk += NWAVE) {
-                    const uint32_t j = blk * 64u + lane;
-                    if (j < c4)
-                        __builtin_amdgcn_global_load_lds((const void*)(src + j), (lds_void*)(lds4 + blk * 64u),
-                                                         16, 0, 0);
-                }
-                o = ld32(a.outcome, loff);
-                load_db();
-                s0 = ld32(a.state, loff);
-                __builtin_amdgcn_s_waitcnt(0);  // chain section in LDS, outcome and word 0 in VGPRs
-                if constexpr (FLOOR) dm = pack(db);
-            } else {
-                for (uint32_t blk = wa; c4 + blk * 64u < n4; blk += NWAVE) {
-                    const uint32_t j = c4 + blk * 64u + lane;
-                    if (j < n4)
-                        __builtin_amdgcn_global_load_lds((const void*)(src + j),
-                                                         (lds_void*)(lds4 + c4 + blk * 64u), 16, 0, 0);
-                }
+            for (uint32_t blk = wa; blk * 64u < c4; blk += NWAVE) {
+                const uint32_t j = blk * 64u + lane;
+                if (j < c4)
+                    __builtin_amdgcn_global_load_lds((const void*)(src + j), (lds_void*)(lds4 + blk * 64u), 16, 0, 0);
             }
-            asm volatile("" ::: "memory");
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            // every lane's words in one place (so that both roles keep them
-            // in the same registers and no copy waits for them); the A lanes
-            // read word 0 a second time
+            o = ld32(a.outcome, loff);
+            load_db();
+            s0 = ld32(a.state, loff);
+            __builtin_amdgcn_s_waitcnt(0);  // chain section in LDS, outcome and word 0 in VGPRs
+            if constexpr (FLOOR) dm = pack(db);
+        };
+        auto stage_b = [&]() {
+            const uint32_t c4 = a.chain_words / 4u;
+            for (uint32_t blk = wa; c4 + blk * 64u < n4; blk += NWAVE) {
+                const uint32_t j = c4 + blk * 64u + lane;
+                if (j < n4)
+                    __builtin_amdgcn_global_load_lds((const void*)(src + j), (lds_void*)(lds4 + c4 + blk * 64u),
+                                                     16, 0, 0);
+            }
+        };
+        // This lane's NW words (unconditional for idle lanes, which read
+        // session 0 and never store, so that no branch splits the loads).
+        auto load_words = [&](auto nw_c) {
+            constexpr int NW = decltype(nw_c)::value;
 #pragma unroll
-            for (int w = 0; w < WH; ++w)
+            for (int w = 0; w < NW; ++w)
                 if (EXACT || wbase + (uint32_t)w < W) S[w] = ld32(a.state + (size_t)(wbase + w) * ldw, loff);
-        } else {
-            // (a1, a2) One lane per session: the first batch of the image,
-            // then the outcome and the state words.  Vector-memory loads
-            // complete in order, so the image batch can be written to LDS
-            // while the state loads are still in flight.
+        };
+        // One lane per session: the first batch of the image, then the
+        // outcome and the state words.  Vector-memory loads complete in
+        // order, so the image batch can be written to LDS while the state
+        // loads are still in flight.
+        auto stage_single = [&]() {
             u32x4* dst = reinterpret_cast<u32x4*>(lds4);
             u32x4 v[SB];
 #pragma unroll
@@ -887,9 +915,7 @@ struct ChainF {
             }
             o = ld32(a.outcome, loff);
             load_db();
-#pragma unroll
-            for (int w = 0; w < WH; ++w)
-                if (EXACT || (uint32_t)w < W) S[w] = ld32(a.state + (size_t)w * ldw, loff);
+            load_words(std::integral_constant<int, WS>{});
             // Blocks past the image end repeat its last block (same value,
             // same address), so the writes need no branch either.
 #pragma unroll
@@ -901,7 +927,7 @@ struct ChainF {
             __syncthreads();
             if constexpr (FLOOR) dm = pack(db);
             s0 = S[0];
-        }
+        };
 
         // per-wavefront constants of the compaction
         const uint32_t in_c = L.s - L.b;
@@ -991,64 +1017,72 @@ struct ChainF {
             }
         };
 
-        chain_chunk(0u);
-        for (uint32_t t0 = 0; t0 < T; t0 += TC) {
+        // Replay of the chunk starting at t0 over this lane's 16-byte word
+        // blocks [QLO, QHI), with (EFF, A lanes) the slots and effects, step
+        // by step.  The LDS reads of step i + 1 (mask blocks and, with EFF,
+        // counts and tool pair) are issued before step i is computed; past
+        // the chunk's last step they read the zero row (valid addresses,
+        // values unused).  The step count is re-read so that no per-step
+        // condition stays live across the phases.
+        auto replay = [&](uint32_t t0, auto qlo_c, auto qhi_c, auto eff_c, auto pref_c) {
+            constexpr int QLO = decltype(qlo_c)::value;
+            constexpr int QHI = decltype(qhi_c)::value;
+            constexpr int NQ = QHI - QLO;
+            constexpr bool EFF = decltype(eff_c)::value;
+            constexpr bool PREF = decltype(pref_c)::value;
+            static_assert(PREF || !EFF, "the effect pass prefetches");
             const uint32_t n = (T - t0) < (uint32_t)TC ? (T - t0) : (uint32_t)TC;
-            if constexpr (MULTI || SPLIT) __syncthreads();
-            if (role_b) {
-#pragma unroll
-                for (int i = 0; i < TC; ++i) {
-                    ctl[i] = lds_x[(2 * i) * (NWAVE * 64) + alane];
-                    add[i] = lds_x[(2 * i + 1) * (NWAVE * 64) + alane];
-                }
-            }
-
-            // replay: this lane's words, and (A lanes) slots and effects, step
-            // by step.  The LDS reads of step i + 1 (mask blocks, counts, tool
-            // pair) are issued before step i is computed; past the chunk's
-            // last step they read the zero row (valid addresses, values
-            // unused).  The step count is re-read so that no per-step
-            // condition stays live across the phases.
             const uint32_t nr = opaque_s(n);
             const uint32_t* cq0 = lds_cnt + (L.flags >> 24);
-            const uint32_t qoff = wbase * 4u;  // byte offset of this lane's first block in a row
-            uint4 mc[NBH];
-            uint32_t cc[4], tpc;
-            {
+            const uint32_t qoff = (wbase + 4u * QLO) * 4u;  // byte offset of the first block in a row
+            uint4 mc[NQ];
+            uint32_t cc[4] = {0u, 0u, 0u, 0u}, tpc = 0u;
+            if constexpr (PREF) {
                 const uint32_t c = ctl[0];
                 const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
 #pragma unroll
-                for (int q = 0; q < NBH; ++q) mc[q] = lds128(lds_rows, rowoff + 16u * q);
+                for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds_rows, rowoff + 16u * q);
+                if constexpr (EFF) {
 #pragma unroll
-                for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[k] : 0u;
-                tpc = lds_tools[c >> 6];
+                    for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[k] : 0u;
+                    tpc = lds_tools[c >> 6];
+                }
             }
 #pragma unroll
             for (int i = 0; i < TC; ++i) {
-                uint4 mn[NBH];
+                uint4 mn[NQ];
                 uint32_t cn[4] = {0u, 0u, 0u, 0u}, tpn = 0u;
-                if (i + 1 < TC) {
+                if constexpr (!PREF) {
+                    const uint32_t c = ctl[i];
+                    const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
+#pragma unroll
+                    for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds_rows, rowoff + 16u * q);
+                }
+                if (PREF && i + 1 < TC) {
                     const uint32_t c = ctl[i + 1];
                     const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
 #pragma unroll
-                    for (int q = 0; q < NBH; ++q) mn[q] = lds128(lds_rows, rowoff + 16u * q);
+                    for (int q = 0; q < NQ; ++q) mn[q] = lds128(lds_rows, rowoff + 16u * q);
+                    if constexpr (EFF) {
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) cn[k] = MULTI ? cq0[(i + 1) * CNT_STRIDE + k] : 0u;
-                    tpn = lds_tools[c >> 6];
+                        for (int k = 0; k < 4; ++k) cn[k] = MULTI ? cq0[(i + 1) * CNT_STRIDE + k] : 0u;
+                        tpn = lds_tools[c >> 6];
+                    }
                 }
                 if ((uint32_t)i < nr) {
                     const uint32_t c = ctl[i];
-                    const bool dk = (c >> 5) & 1u;
                     const uint32_t oo = add[i];
 #pragma unroll
-                    for (int q = 0; q < NBH; ++q) {
-                        if (!EXACT && wbase + (uint32_t)(4 * q) >= W) continue;
-                        S[4 * q] = (rotr32(S[4 * q], c) ^ mc[q].x) + oo;
-                        S[4 * q + 1] = (rotr32(S[4 * q + 1], c) ^ mc[q].y) + oo;
-                        S[4 * q + 2] = (rotr32(S[4 * q + 2], c) ^ mc[q].z) + oo;
-                        S[4 * q + 3] = (rotr32(S[4 * q + 3], c) ^ mc[q].w) + oo;
+                    for (int q = 0; q < NQ; ++q) {
+                        const int b = 4 * (QLO + q);
+                        if (!EXACT && wbase + (uint32_t)b >= W) continue;
+                        S[b] = (rotr32(S[b], c) ^ mc[q].x) + oo;
+                        S[b + 1] = (rotr32(S[b + 1], c) ^ mc[q].y) + oo;
+                        S[b + 2] = (rotr32(S[b + 2], c) ^ mc[q].z) + oo;
+                        S[b + 3] = (rotr32(S[b + 3], c) ^ mc[q].w) + oo;
                     }
-                    if (!role_b) {
+                    if constexpr (EFF) {
+                        const bool dk = (c >> 5) & 1u;
                         const uint32_t tool = (tpc >> (dk ? 8u : 0u)) & 7u;
 
                         // (a5) stable partition, taken first
@@ -1081,31 +1115,107 @@ struct ChainF {
                         p_cnt += a.n_cohorts;
                     }
                 }
-                if (i + 1 < TC) {
+                if (PREF && i + 1 < TC) {
 #pragma unroll
-                    for (int q = 0; q < NBH; ++q) mc[q] = mn[q];
+                    for (int q = 0; q < NQ; ++q) mc[q] = mn[q];
+                    if constexpr (EFF) {
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) cc[k] = cn[k];
-                    tpc = tpn;
+                        for (int k = 0; k < 4; ++k) cc[k] = cn[k];
+                        tpc = tpn;
+                    }
                 }
             }
-            // the counts and the control buffer are rewritten by the next
-            // chunk only after every wavefront has finished reading them
-            if (t0 + TC < T) {
-                if constexpr (MULTI || SPLIT) __syncthreads();
-                chain_chunk(t0 + TC);
-            }
-        }
+        };
 
-        // (a9) store the state and (A lanes) the next outcome (the row
-        // addresses are recomputed from a fresh copy of ld rather than kept
-        // live across the chain)
-        if (L.active) {
-            const uint32_t ld_st = opaque_s(a.ld);
+        // (a9) store this lane's NW words and (A lanes) the next outcome (the
+        // row addresses are recomputed from a fresh copy of ld rather than
+        // kept live across the chain)
+        auto store_state = [&](auto nw_c, bool with_outcome) {
+            constexpr int NW = decltype(nw_c)::value;
+            if (L.active) {
+                const uint32_t ld_st = opaque_s(a.ld);
 #pragma unroll
-            for (int w = 0; w < WH; ++w)
-                if (EXACT || wbase + (uint32_t)w < W) st32<true>(a.state + (size_t)(wbase + w) * ld_st, soff, S[w]);
-            if (!role_b) st32<true>(a.outcome, soff, o);
+                for (int w = 0; w < NW; ++w)
+                    if (EXACT || wbase + (uint32_t)w < W) st32<true>(a.state + (size_t)(wbase + w) * ld_st, soff, S[w]);
+                if (with_outcome) st32<true>(a.outcome, soff, o);
+            }
+        };
+        auto bare_barrier = []() {
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+        };
+        using Z = std::integral_constant<int, 0>;
+        using NA = std::integral_constant<int, NBA>;
+        using NB = std::integral_constant<int, NBB>;
+        using Yes = std::integral_constant<bool, true>;
+        using No = std::integral_constant<bool, false>;
+        // the B lanes of a 28-word split read each step's masks when the step
+        // starts (no room for a second set of mask registers)
+        using PrefB = std::integral_constant<bool, (NBB <= 4)>;
+
+        // Each role runs its own straight-line sequence to the end, with the
+        // same barriers per chunk, so that the compiler's wait analysis sees
+        // one role's accesses at a time.  Chunk 0 runs outside the chunk
+        // loop: the compiler flushes every outstanding vector-memory access
+        // in the preheader of a loop that stores without loading.
+        if constexpr (SPLIT) {
+            if (!role_b) {
+                stage_a();
+                bare_barrier();
+                load_words(std::integral_constant<int, WA>{});
+                chain_chunk(0u);
+                lds_barrier();  // publishes chunk 0's counts and control
+                // The replay needs all WA words at its first step; an explicit
+                // wait here (nothing else is outstanding) keeps the compiler
+                // from repeating it, step after step, behind the effect stores.
+                wait_vmcnt<0>();
+                replay(0u, Z{}, NA{}, Yes{}, Yes{});
+                for (uint32_t t0 = TC; t0 < T; t0 += TC) {
+                    lds_barrier();  // every wavefront is done with the previous chunk's
+                    chain_chunk(t0);
+                    lds_barrier();
+                    replay(t0, Z{}, NA{}, Yes{}, Yes{});
+                }
+                store_state(std::integral_constant<int, WA>{}, true);
+            } else {
+                stage_b();
+                bare_barrier();
+                load_words(std::integral_constant<int, WB>{});
+                // the row loads issued before the WB state loads have landed
+                // (with W < WMAX fewer state loads were issued: wait for all)
+                wait_vmcnt<EXACT ? WB : 0>();
+                lds_barrier();
+                auto read_ctl = [&]() {
+#pragma unroll
+                    for (int i = 0; i < TC; ++i) {
+                        ctl[i] = lds_x[(2 * i) * (NWAVE * 64) + alane];
+                        add[i] = lds_x[(2 * i + 1) * (NWAVE * 64) + alane];
+                    }
+                };
+                read_ctl();
+                wait_vmcnt<0>();  // every word is needed at the first step
+                replay(0u, Z{}, NB{}, No{}, PrefB{});
+                for (uint32_t t0 = TC; t0 < T; t0 += TC) {
+                    lds_barrier();
+                    lds_barrier();
+                    read_ctl();
+                    replay(t0, Z{}, NB{}, No{}, PrefB{});
+                }
+                store_state(std::integral_constant<int, WB>{}, false);
+            }
+        } else {
+            stage_single();
+            chain_chunk(0u);
+            if constexpr (MULTI) lds_barrier();
+            replay(0u, Z{}, NA{}, Yes{}, Yes{});
+            for (uint32_t t0 = TC; t0 < T; t0 += TC) {
+                if constexpr (MULTI) lds_barrier();
+                chain_chunk(t0);
+                if constexpr (MULTI) lds_barrier();
+                replay(t0, Z{}, NA{}, Yes{}, Yes{});
+            }
+            store_state(std::integral_constant<int, WMAX>{}, true);
         }
     }
 };
