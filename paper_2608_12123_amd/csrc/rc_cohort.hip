@@ -851,7 +851,7 @@ struct ChainF {
             for (int i = 0; i < TC; ++i) m |= ((w[i] >> (L.s & 31u)) & 1u) << i;
             return L.active ? m : 0u;
         };
-        uint32_t dm = 0u;
+        uint32_t dm = 0u, dm1 = 0u;
         // FLOOR: decision words, issued before the state words so that the
         // chain waits only for them and word 0
         auto load_db = [&]() {
@@ -879,10 +879,8 @@ struct ChainF {
                     __builtin_amdgcn_global_load_lds((const void*)(src + j), (lds_void*)(lds4 + blk * 64u), 16, 0, 0);
             }
             o = ld32(a.outcome, loff);
-            load_db();
             s0 = ld32(a.state, loff);
             __builtin_amdgcn_s_waitcnt(0);  // chain section in LDS, outcome and word 0 in VGPRs
-            if constexpr (FLOOR) dm = pack(db);
         };
         auto stage_b = [&]() {
             const uint32_t c4 = a.chain_words / 4u;
@@ -966,8 +964,12 @@ struct ChainF {
                 // wavefronts of the SIMD replay (throughput work that fills
                 // the gaps).
                 __builtin_amdgcn_s_setprio(3);
-                if constexpr (FLOOR)
-                    if (t0 != 0u) dm = pack(db);
+                if constexpr (FLOOR) {
+                    if (SPLIT && t0 == (uint32_t)TC)
+                        dm = dm1;  // packed before the first chunk
+                    else if (t0 != 0u)
+                        dm = pack(db);
+                }
                 // chain: word 0 only
                 uint32_t r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
                 uint32_t m0 = lds[r];  // taken mask of word 0 on route r (chain section)
@@ -990,9 +992,9 @@ struct ChainF {
                     step += 1u;
                 }
                 // FLOOR: the next chunk's decision words, in flight during
-                // this chunk's replay
+                // this chunk's replay (SPLIT: chunk 1's are already packed)
                 if constexpr (FLOOR) {
-                    if (t0 + (uint32_t)TC < T) {
+                    if ((!SPLIT || t0 >= (uint32_t)TC) && t0 + (uint32_t)TC < T) {
 #pragma unroll
                         for (int i = 0; i < TC; ++i)
                             db[i] = t0 + (uint32_t)(TC + i) < T ? dword_of(a, t0 + TC + i, L.active ? L.s : 0u) : 0u;
@@ -1163,7 +1165,23 @@ struct ChainF {
             if (!role_b) {
                 stage_a();
                 bare_barrier();
+                // FLOOR: the decision words of the first two chunks go out
+                // after the barrier (so that the other wavefronts are not held
+                // at it while they arrive) and are packed before any store is
+                // issued: once stores are outstanding, waiting for a load
+                // drains them too.
+                load_db();
+                uint32_t db1[TC];
+                if constexpr (FLOOR) {
+#pragma unroll
+                    for (int i = 0; i < TC; ++i)
+                        db1[i] = (uint32_t)(TC + i) < T ? dword_of(a, (uint32_t)(TC + i), L.active ? L.s : 0u) : 0u;
+                }
                 load_words(std::integral_constant<int, WA>{});
+                if constexpr (FLOOR) {
+                    dm = pack(db);
+                    dm1 = pack(db1);
+                }
                 chain_chunk(0u);
                 lds_barrier();  // publishes chunk 0's counts and control
                 // The replay needs all WA words at its first step; an explicit
