@@ -92,6 +92,10 @@ FLOOR_SWEEP = [
     (48, 1000, wk.ROUTE_MOD, [128, 128, 64, 64, 32, 32, 3], 6, 0, 0.2),
     (64, 1024, wk.ROUTE_CDF, [256, 1, 255, 129, 127, 64, 33], 5, 7, 0.05),
     (64, 200, wk.ROUTE_MOD, [256] * 3 + [31], 9, 0, 0.6),
+    # two lanes per session: beyond the two chunks whose decisions are
+    # loaded up front, and W < 32
+    (32, 128, wk.ROUTE_CDF, [256] * 3 + [200, 17], 40, 0, 0.4),
+    (20, 8, wk.ROUTE_MOD, [256, 40, 90], 33, 5, 0.7),
 ]
 
 

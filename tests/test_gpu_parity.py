@@ -103,6 +103,9 @@ SWEEP = [
     (63, 5, wk.ROUTE_MOD, 32768, [1] * 70 + [256], 2, 2, 0),
     (64, 1024, wk.ROUTE_CDF, 3277, [256, 1, 255, 129, 127, 64, 33], 5, 0, 12345),
     (64, 256, wk.ROUTE_MOD, 32768, [256] * 3, 16, 0, 0),
+    # two lanes per session with W < 32, three chunks of steps
+    (24, 32, wk.ROUTE_MOD, 30000, [256, 100, 64, 33, 256], 40, 3, 5),
+    (32, 128, wk.ROUTE_CDF, 19661, [256] * 3 + [200, 17], 37, 0, 0),
 ]
 
 
