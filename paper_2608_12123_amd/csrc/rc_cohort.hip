@@ -973,19 +973,26 @@ struct ChainF {
                 // chain: word 0 only
                 uint32_t r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
                 uint32_t m0 = lds[r];  // taken mask of word 0 on route r (chain section)
+                // Branch-free: the decision is a lane mask, and the taken and
+                // not-taken forms of the update differ only in masked
+                // operands (a select the compiler would otherwise turn into a
+                // divergent branch on this latency-bound path).
+                const uint32_t act = L.active ? 1u : 0u;
 #pragma unroll
                 for (int i = 0; i < TC; ++i) {
                     if ((uint32_t)i >= n) continue;
-                    bool dk;
+                    uint32_t dbit;
                     if constexpr (FLOOR)
-                        dk = (dm >> i) & 1u;
+                        dbit = (dm >> i) & 1u;
                     else
-                        dk = L.active && ((dev_fmix32(s0 ^ o ^ step) & 0xFFFFu) < a.thr);
+                        dbit = act & (uint32_t)((dev_fmix32(s0 ^ o ^ step) & 0xFFFFu) < a.thr);
+                    const uint32_t dmsk = 0u - dbit;  // all ones when taken
                     const uint32_t sh = (31u - r) & 31u;
-                    const uint32_t oo = opaque(dk ? 0u : o);
-                    ctl[i] = (dk ? 32u : sh) | (r << 6);  // rotation 0 when taken
+                    const uint32_t rot = sh & ~dmsk;  // rotation 0 when taken
+                    const uint32_t oo = o & ~dmsk;
+                    ctl[i] = rot | (dmsk & 32u) | (r << 6);
                     add[i] = oo;
-                    s0 = (rotr32(s0, dk ? 0u : sh) ^ (dk ? m0 : 0u)) + oo;
+                    s0 = (rotr32(s0, rot) ^ (m0 & dmsk)) + oo;
                     o = dev_fmix32(s0);
                     r = route_of<RK>(o, a.ra, lds + a.cdf_off, lds + a.guide_off);
                     m0 = lds[r];
