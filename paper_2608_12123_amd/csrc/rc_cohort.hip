@@ -733,6 +733,27 @@ struct Chain {
     }
 };
 
+// Workgroup barrier for LDS traffic only: each wavefront waits for its own
+// LDS accesses (lgkmcnt 0; vmcnt and expcnt left at their maxima), not for
+// its global loads and stores, which no other wavefront reads -- so state
+// loads stay in flight across it.  (A workgroup release fence would wait for
+// every outstanding global access as well.)
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Wait until at most N vector-memory accesses of this wavefront are
+// outstanding (lgkmcnt and expcnt unconstrained).  They complete in issue
+// order, so this waits for everything issued before the last N.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N <= 63, "vmcnt is a 6-bit count");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // Full-image chain, split by what each word depends on.  A session's route,
 // decision and next outcome at every step are functions of word 0 and the
 // outcome alone; every other word only follows the per-step (mask row,
@@ -746,39 +767,17 @@ struct Chain {
 //            LDS read and two VALU ops per four words), the stable-partition
 //            slot, and the effect stores.
 // SPLIT: two lanes per session.  Wavefronts [0, NWAVE) ("A") run the plan's
-// sessions: the chain, words [0, W/2), the slots and the effects.
+// sessions: the chain, words [0, WA), the slots and the effects.
 // Wavefronts [NWAVE, 2 NWAVE) ("B") mirror them lane for lane and replay
-// words [W/2, W) from the control the A lanes leave in LDS before the
-// chunk's barrier; a second barrier closes the chunk when another follows.
-// A lone wavefront issues VALU work at about half the rate a SIMD sustains
-// with several, so the second wavefront per session roughly halves the
-// replay.
-// Workgroup barrier for LDS traffic only: each wavefront waits for its own
-// LDS accesses (lgkmcnt 0; vmcnt and expcnt left at their maxima), not for
-// its global loads and stores, which no other wavefront reads -- so state
-// loads stay in flight across it.  (A workgroup release fence would wait for
-// every outstanding global access as well.)
-// Wait until at most N vector-memory accesses of this wavefront are
-// outstanding (lgkmcnt and expcnt unconstrained).  They complete in issue
-// order, so this waits for everything issued before the last N.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N <= 63, "vmcnt is a 6-bit count");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
+// words [WA, W) from the control the A lanes leave in LDS before the chunk's
+// barrier; a second barrier closes the chunk when another follows.  The two
+// roles run separate straight-line sequences with the same barriers.
 // Rows of the mask image are W + 4 words apart (one zero block of padding
 // shifts consecutive rows across the LDS banks), so block q of a row is an
 // immediate offset from the row's byte offset.
 // FLOOR: the no-decision floor -- the A lanes read every decision from the
-// bitmap (each chunk's words loaded a chunk ahead) instead of computing it.
+// bitmap instead of computing it (SPLIT: the first two chunks' words loaded
+// after the first barrier, later chunks' a chunk ahead).
 template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT, bool FLOOR>
 struct ChainF {
     // Effect stores stay on the normal path: cohorts spanning wavefronts
@@ -834,9 +833,9 @@ struct ChainF {
         const uint32_t loff = L.active ? soff : 0u;
         const uint32_t ldw = opaque_s(a.ld);
         uint32_t o = 0u;
-        // Word 0 of the chain (A lanes) in a variable of its own: on the B
-        // path it is a constant, so no wait for outstanding state loads is
-        // attached to it where the two paths join.
+        // Word 0 of the chain (A lanes) in a variable of its own: it is
+        // loaded with the outcome before the first barrier, apart from the
+        // state words that follow it.
         uint32_t s0 = 0u;
         uint32_t db[TC];  // FLOOR: the decision words of the first chunk (A lanes)
 #pragma unroll
