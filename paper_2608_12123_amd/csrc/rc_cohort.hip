@@ -14,17 +14,19 @@
 //
 // Data layout (HBM, structure of arrays, leading dimension ld): state
 // [W][ld], outcome [ld], effects [T][ld] for sid and tool, [T][ld][4] for the
-// payload, n_taken [T][C].  A wavefront's 64 lanes read 64 consecutive
-// sessions of one word row (a 256-byte segment); an effect's payload is one
-// 16-byte store.
+// payload, n_taken [T][C].  A wavefront's lanes read the consecutive
+// sessions of each of its cohorts from one word row (at most a few
+// contiguous segments per row); an effect's payload is one 16-byte store.
 //
 // Launch plan (built on the host at create time).  Cohorts of at most 64
 // sessions are packed, in order, into "sub-wavefront" bins that never need a
-// workgroup barrier; larger cohorts go, in order, into "multi-wavefront"
-// bins.  A bin is one workgroup of 4 or 8 wavefronts.  A cohort of at most 64
-// sessions never straddles a wavefront; a larger one starts on a wavefront
-// boundary and spans whole wavefronts; no cohort straddles a bin.  Each
-// wavefront has a 32-byte descriptor read with scalar loads.  The compaction
+// workgroup barrier -- each into the first wavefront of the open bin with room
+// for it, so a wavefront can hold several cohorts that are not neighbours --
+// and larger cohorts go, in order, into "multi-wavefront" bins.  A bin is one
+// workgroup of 4 or 8 wavefronts.  A cohort of at most 64 sessions never
+// straddles a wavefront; a larger one starts on a wavefront boundary and spans
+// whole wavefronts; no cohort straddles a bin.  Each wavefront has a 64-byte
+// descriptor read with scalar loads.  The compaction
 // (stable partition, taken first) is a wavefront ballot + mbcnt rank; a
 // cohort spanning wavefronts adds an LDS exchange of per-wavefront popcounts
 // behind one workgroup barrier per step.
@@ -176,16 +178,19 @@ __device__ __forceinline__ void st128(uint32_t* base, uint32_t byte_off, uint4 v
     else *p = x;
 }
 
-// Wavefront descriptor of the launch plan (8 x u32).
+// Wavefront descriptor of the launch plan (16 x u32).
 enum : uint32_t {
     WD_S0 = 0,        // session of lane 0
-    WD_NACT = 1,      // lanes [0, n_act) hold sessions s0 .. s0 + n_act - 1
+    WD_NACT = 1,      // lanes [0, n_act) are active
     WD_CFIRST = 2,    // cohort of lane 0
     WD_NCOH = 3,      // cohorts present in this wavefront
     WD_BFIRST = 4,    // first session of cohort c_first
     WD_KFIRST = 5,    // size of cohort c_first
     WD_FLAGS = 6,
-    WD_WORDS = 8
+    WD_LIST = 8,      // sub-wavefront cohorts, in lane order: cohort q takes the
+                      // next k_q lanes, which hold its sessions in order
+    WD_MAXC = 8,      // at most this many cohorts per wavefront
+    WD_WORDS = 16
 };
 enum : uint32_t {
     WF_MULTI = 1u,    // this wavefront is part of a cohort of > 64 sessions
@@ -273,21 +278,29 @@ __device__ __forceinline__ LaneCohort lane_cohort(const uint32_t* __restrict__ w
     L.flags = uni(wd[WD_FLAGS]);
     L.s = s0 + lane;
     L.c = c_first;
+    uint32_t lo = 0u;  // first lane of this lane's cohort
     if (n_coh > 1u) {
-        // several sub-wavefront cohorts: find this lane's one
-        for (uint32_t q = 1; q < n_coh; ++q) {
-            const uint32_t bq = offsets[c_first + q];  // uniform address
-            L.c = (bq <= L.s) ? c_first + q : L.c;
+        // several sub-wavefront cohorts, listed in lane order: this lane's
+        // is the last one that starts at or before it
+        uint32_t at = 0u;
+        for (uint32_t q = 0; q < n_coh; ++q) {
+            const uint32_t cq = uni(wd[WD_LIST + q]);
+            const uint32_t bq = offsets[cq];  // uniform addresses
+            const uint32_t kq = offsets[cq + 1u] - bq;
+            const bool mine = lane >= at;
+            L.c = mine ? cq : L.c;
+            b = mine ? bq : b;
+            k = mine ? kq : k;
+            lo = mine ? at : lo;
+            at += kq;
         }
-        b = offsets[L.c];
-        k = offsets[L.c + 1u] - b;
+        L.s = b + (lane - lo);
     }
     L.b = b;
     L.k = k;
     L.active = lane < n_act && L.c >= cb && L.c < ce;
     L.seg = 0;
     if (!(L.flags & WF_MULTI)) {
-        uint32_t lo = b - s0;
         uint32_t hi = lo + k;
         lo = lo < 64u ? lo : 64u;
         hi = hi < 64u ? hi : 64u;
@@ -1552,9 +1565,10 @@ int validate_desc(const rc_cohort_desc* d) {
 }
 
 // Pack cohorts into bins of nw wavefronts (see the file comment): first every
-// cohort of at most 64 sessions, in order, then the larger ones.  Lanes of a
-// wavefront hold consecutive sessions, so two small cohorts share a
-// wavefront only when they are consecutive cohorts.
+// cohort of at most 64 sessions, in order, each into the first wavefront of
+// the open bin with room for it (at most WD_MAXC cohorts per wavefront), then
+// the larger ones.  A cohort never goes to an earlier bin than the one
+// before it, so the bins of a cohort range are contiguous.
 void build_plan(const uint32_t* off, uint32_t C, uint32_t nw_per_bin, Plan& P) {
     const uint32_t NW = nw_per_bin;
     P.nwave = NW;
@@ -1562,37 +1576,68 @@ void build_plan(const uint32_t* off, uint32_t C, uint32_t nw_per_bin, Plan& P) {
     P.bin_of_cohort.assign(C, 0);
     int64_t bin = -1;        // open bin (-1: none)
     uint32_t wave = 0, lane = 0;
-    uint32_t prev_c = 0;     // last cohort placed in the open wavefront (lane > 0)
+    // sub-wavefront class: free lanes and cohorts of the open bin's wavefronts
+    std::vector<uint32_t> room(NW, 0u), ncoh(NW, 0u);
+    uint32_t started = 0;    // wavefronts started in the open bin
+    // multi-wavefront class: the bin before the open one, still open
+    int64_t prev_bin = -1;
+    uint32_t prev_used = 0;
     auto open_bin = [&]() {
         ++bin;
         wave = 0;
         lane = 0;
+        started = 0;
         P.wdesc.resize((size_t)(bin + 1) * NW * WD_WORDS, 0u);
     };
     auto place = [&](uint32_t c) {
         const uint32_t b = off[c], k = off[c + 1] - off[c];
         if (k > 64u) {
+            // The previous bin stays open beside the current one: a cohort
+            // goes into the first of the two with nw free wavefronts left,
+            // else into a new bin (which retires the previous one).  So a
+            // cohort lands at most one bin before the one of any cohort
+            // placed earlier; bins_of_range widens its range by one.
             const uint32_t nw = (k + 63u) / 64u;
-            if (lane > 0u) { ++wave; lane = 0; }
-            if (bin < 0 || wave + nw > NW) open_bin();
+            int64_t tb;
+            uint32_t tw;
+            if (prev_bin >= 0 && prev_used + nw <= NW) {
+                tb = prev_bin;
+                tw = prev_used;
+                prev_used += nw;
+            } else {
+                if (bin < 0 || wave + nw > NW) {
+                    prev_bin = bin;  // -1 before the class's first bin
+                    prev_used = wave;
+                    open_bin();
+                }
+                tb = bin;
+                tw = wave;
+                wave += nw;
+            }
             for (uint32_t i = 0; i < nw; ++i) {
-                uint32_t* d = &P.wdesc[((size_t)bin * NW + wave + i) * WD_WORDS];
+                uint32_t* d = &P.wdesc[((size_t)tb * NW + tw + i) * WD_WORDS];
                 d[WD_S0] = b + 64u * i;
                 d[WD_NACT] = (k - 64u * i) < 64u ? (k - 64u * i) : 64u;
                 d[WD_CFIRST] = c;
                 d[WD_NCOH] = 1;
                 d[WD_BFIRST] = b;
                 d[WD_KFIRST] = k;
-                d[WD_FLAGS] = WF_MULTI | (i << 8) | (nw << 16) | (wave << 24);
+                d[WD_FLAGS] = WF_MULTI | (i << 8) | (nw << 16) | (tw << 24);
             }
-            P.bin_of_cohort[c] = (uint32_t)bin;
-            wave += nw;
-            lane = 0;
+            P.bin_of_cohort[c] = (uint32_t)tb;
         } else {
-            if (lane > 0u && (lane + k > 64u || c != prev_c + 1u)) { ++wave; lane = 0; }
-            if (bin < 0 || wave >= NW) open_bin();
-            uint32_t* d = &P.wdesc[((size_t)bin * NW + wave) * WD_WORDS];
-            if (lane == 0u) {
+            // first fit among the wavefronts of the open bin (so that the
+            // bins of a cohort range stay together), then a new wavefront
+            uint32_t w = NW;
+            if (bin >= 0)
+                for (uint32_t q = 0; q < started; ++q)
+                    if (room[q] >= k && ncoh[q] < WD_MAXC) { w = q; break; }
+            if (w == NW) {
+                if (bin < 0 || started == NW) open_bin();
+                w = started++;
+                room[w] = 64u;
+                ncoh[w] = 0u;
+                uint32_t* d = &P.wdesc[((size_t)bin * NW + w) * WD_WORDS];
                 d[WD_S0] = b;
                 d[WD_NACT] = 0;
                 d[WD_CFIRST] = c;
@@ -1601,11 +1646,12 @@ void build_plan(const uint32_t* off, uint32_t C, uint32_t nw_per_bin, Plan& P) {
                 d[WD_KFIRST] = k;
                 d[WD_FLAGS] = 0;
             }
+            uint32_t* d = &P.wdesc[((size_t)bin * NW + w) * WD_WORDS];
+            d[WD_LIST + ncoh[w]] = c;
+            d[WD_NCOH] = ++ncoh[w];
             d[WD_NACT] += k;
-            d[WD_NCOH] += 1;
+            room[w] -= k;
             P.bin_of_cohort[c] = (uint32_t)bin;
-            lane += k;
-            prev_c = c;
         }
     };
     for (uint32_t c = 0; c < C; ++c)
@@ -1613,6 +1659,7 @@ void build_plan(const uint32_t* off, uint32_t C, uint32_t nw_per_bin, Plan& P) {
     P.n_bins_a = (uint32_t)(bin + 1);
     wave = NW;  // the multi-wavefront class starts in a fresh bin
     lane = 0;
+    prev_bin = -1;
     for (uint32_t c = 0; c < C; ++c)
         if (off[c + 1] - off[c] > 64u) place(c);
     P.n_bins = (uint32_t)(bin + 1);
@@ -1660,9 +1707,15 @@ void bins_of_range(const Plan& P, uint32_t cb, uint32_t ce, uint32_t& a_lo, uint
     }
     const uint32_t fb = P.first_b[cb];
     if (fb < ce) {
+        // a multi-wavefront cohort lies at most one bin before the bin of
+        // any cohort placed earlier (build_plan), so the range's cohorts lie
+        // within one bin of [bin(first), bin(last)]; cohorts of the extra
+        // bins outside [cb, ce) are masked off in the kernels
         const uint32_t lb = (uint32_t)P.last_b[ce - 1];
-        b_lo = P.bin_of_cohort[fb];
-        b_n = P.bin_of_cohort[lb] - b_lo + 1u;
+        const uint32_t lo = P.bin_of_cohort[fb] > P.n_bins_a ? P.bin_of_cohort[fb] - 1u : P.n_bins_a;
+        const uint32_t hi = P.bin_of_cohort[lb] + 1u < P.n_bins ? P.bin_of_cohort[lb] + 1u : P.n_bins - 1u;
+        b_lo = lo;
+        b_n = hi - lo + 1u;
     }
 }
 
@@ -2064,10 +2117,19 @@ int rc_plan_lanes(const rc_cohort_desc* desc, uint32_t lanes_per_workgroup, uint
         const uint32_t* d = &P.wdesc[(size_t)wv * WD_WORDS];
         for (uint32_t lane = 0; lane < 64u; ++lane) {
             // the per-lane derivation of lane_cohort() in the kernels
-            const uint32_t s = d[WD_S0] + lane;
+            uint32_t s = d[WD_S0] + lane;
             uint32_t c = d[WD_CFIRST];
-            for (uint32_t q = 1; q < d[WD_NCOH]; ++q)
-                if (off[d[WD_CFIRST] + q] <= s) c = d[WD_CFIRST] + q;
+            if (d[WD_NCOH] > 1u) {
+                uint32_t at = 0u;
+                for (uint32_t q = 0; q < d[WD_NCOH]; ++q) {
+                    const uint32_t cq = d[WD_LIST + q];
+                    if (lane >= at) {
+                        c = cq;
+                        s = off[cq] + (lane - at);
+                    }
+                    at += off[cq + 1u] - off[cq];
+                }
+            }
             const bool act = lane < d[WD_NACT];
             lane_session[wv * 64u + lane] = act ? s : 0xFFFFFFFFu;
             lane_cohort_out[wv * 64u + lane] = act ? c : 0xFFFFFFFFu;
