@@ -329,9 +329,12 @@ def cpu_baseline(inp, T, min_seconds):
                          os.cpu_count() or 0)}, first
 
 
-def oracle_call_times(orc, inp, T, seconds):
+def oracle_call_times(orc, inp, T, seconds, n_threads=1):
     """Seconds per call of the oracle's C entry point on preallocated buffers
-    (one direct ctypes call per sample, no Python-side copies)."""
+    (one direct ctypes call per sample, no Python-side copies).  With
+    n_threads > 1 the cohorts are split into that many contiguous ranges,
+    each run by the unchanged oracle on its own host thread (ctypes releases
+    the GIL; cohorts write disjoint outputs)."""
     import ctypes
     p32 = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
     state, outcome = inp.state.copy(), inp.outcome.copy()
@@ -348,10 +351,21 @@ def oracle_call_times(orc, inp, T, seconds):
     fn = orc.lib.rc_oracle_run_chain
     out = []
     t_end = time.perf_counter() + seconds
-    while len(out) < 5 or time.perf_counter() < t_end:
-        t0 = time.perf_counter()
-        fn(*args)
-        out.append(time.perf_counter() - t0)
+    if n_threads <= 1:
+        while len(out) < 5 or time.perf_counter() < t_end:
+            t0 = time.perf_counter()
+            fn(*args)
+            out.append(time.perf_counter() - t0)
+        return out
+    from concurrent.futures import ThreadPoolExecutor
+    C = inp.n_cohorts
+    cuts = [C * i // n_threads for i in range(n_threads + 1)]
+    parts = [args[:18] + (cuts[i], cuts[i + 1], None) for i in range(n_threads) if cuts[i] < cuts[i + 1]]
+    with ThreadPoolExecutor(len(parts)) as ex:
+        while len(out) < 5 or time.perf_counter() < t_end:
+            t0 = time.perf_counter()
+            list(ex.map(lambda a: fn(*a), parts))
+            out.append(time.perf_counter() - t0)
     return out
 
 
@@ -364,19 +378,24 @@ def safe_suffix_threshold(rc, wk, sizes=KR_SIZES, steps=KR_STEPS, gpu_reps=200, 
     the hardware threshold"): the start of a measured safe suffix -- the
     smallest tested batch size from which every larger tested size is faster
     on the device-resident chain than on the named baseline, here the
-    single-threaded oracle on the host cores.
+    single-threaded oracle on the host cores, and an all-core bound.
 
     A batch of K sessions is one invocation over cohorts of min(K, 256)
     sessions (W = 32, R = 64 Zipf(1.1) routes, p = 0.3: the K = 256
     workload's shape), chained T steps.  GPU: median microseconds of one
     synchronized invocation (launch, run, stream sync: the latency an online
-    caller sees).  CPU: median microseconds of the oracle on the same inputs.
-    K_r is null when even the largest tested size is not faster."""
+    caller sees).  CPU: median microseconds of the oracle on the same inputs;
+    all cores: that time divided by min(cores, cohorts) -- perfect scaling
+    over independent cohorts, an optimistic bound for the host, checked
+    against a measured multi-threaded run at the largest K.  K_r is null
+    when even the largest tested size is not faster."""
     import torch
     import oracle
     orc = oracle.load()
     stream = torch.cuda.current_stream().cuda_stream
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
     rows = []
+    check = None
     for K in sizes:
         cs = min(K, 256)
         inp = wk.make_custom(n_words=32, n_routes=64, route_mode=wk.ROUTE_CDF, decide_thr=19661,
@@ -397,25 +416,35 @@ def safe_suffix_threshold(rc, wk, sizes=KR_SIZES, steps=KR_STEPS, gpu_reps=200, 
                     rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_RESIDENT, 0, inp.n_cohorts, stream)
                     torch.cuda.current_stream().synchronize()
                     g.append(time.perf_counter() - t0)
-                c = oracle_call_times(orc, inp, T, cpu_seconds)
+                c = float(np.median(oracle_call_times(orc, inp, T, cpu_seconds)))
                 rows.append({"K": K, "T": T, "gpu_us": round(float(np.median(g)) * 1e6, 2),
-                             "cpu_us": round(float(np.median(c)) * 1e6, 2)})
+                             "cpu_us": round(c * 1e6, 2),
+                             "cpu_all_us": round(c / min(cores, inp.n_cohorts) * 1e6, 2)})
+                if K == max(sizes) and T == 16:
+                    n = min(cores, inp.n_cohorts)
+                    m = float(np.median(oracle_call_times(orc, inp, T, 10 * cpu_seconds, n_threads=n)))
+                    check = {"K": K, "T": T, "threads": n, "measured_us": round(m * 1e6, 2),
+                             "bound_us": round(c / n * 1e6, 2)}
         finally:
             rc.rc_cohort_destroy(h)
-    k_r = {}
-    for T in steps:
-        r = sorted((x for x in rows if x["T"] == T), key=lambda x: x["K"])
-        kr = None
-        for x in reversed(r):
-            if x["gpu_us"] < x["cpu_us"]:
-                kr = x["K"]
-            else:
-                break
-        k_r[str(T)] = kr
-    return {"k_r_by_T": k_r, "rows": rows,
+    def threshold(key):
+        k_r = {}
+        for T in steps:
+            r = sorted((x for x in rows if x["T"] == T), key=lambda x: x["K"])
+            kr = None
+            for x in reversed(r):
+                if x["gpu_us"] < x[key]:
+                    kr = x["K"]
+                else:
+                    break
+            k_r[str(T)] = kr
+        return k_r
+    return {"k_r_by_T": threshold("cpu_us"), "k_r_by_T_all_cores": threshold("cpu_all_us"),
+            "cores": cores, "all_core_check": check, "rows": rows,
             "note": "smallest tested K from which every larger tested K is faster on the resident "
-                    "chain (synchronized invocation) than on the single-threaded oracle; cohorts "
-                    "of min(K, 256) sessions, W=32, R=64 Zipf(1.1), p=0.3"}
+                    "chain (synchronized invocation) than on the single-threaded oracle (k_r_by_T) "
+                    "or on its all-core bound (k_r_by_T_all_cores); cohorts of min(K, 256) "
+                    "sessions, W=32, R=64 Zipf(1.1), p=0.3"}
 
 
 ONLINE_CAPACITY = 4096  # queue capacity per route of the online compactor
