@@ -80,6 +80,31 @@ def stored_traffic(workload_key):
         return None
 
 
+PROFILE_VALU = os.path.join(ROOT, "profiles", "rc_chain_kernel_%s_valu.txt")  # by workload
+ENGINE_CLOCK_HZ = 2.4e9  # MI355X peak engine clock
+
+
+def stored_valu(workload_key):
+    """VALU instructions per launch of the workload from the committed
+    rocprofv3 counter summary, valid only while the kernel source is
+    unchanged (None otherwise)."""
+    path = PROFILE_VALU % workload_key
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_src_sha256_16") != kernel_src_hash():
+        return None
+    try:
+        return {"insts_per_launch": int(vals["SQ_INSTS_VALU"]), "waves": int(vals["SQ_WAVES"])}
+    except (KeyError, ValueError):
+        return None
+
+
 class Sets:
     """Rotating device buffer sets for one handle."""
 
@@ -218,9 +243,22 @@ def time_hrt(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
     return time.perf_counter() - t0
 
 
+MECH_ROWS = 9  # timed rows per mechanism and workload (median reported)
+
+
+def _rows(timed, n_per_row, rows=MECH_ROWS):
+    """Microseconds per invocation of `rows` timed rows of n_per_row
+    invocations each: (median, 10th percentile, 90th percentile)."""
+    us = [timed(n_per_row) / n_per_row * 1e6 for _ in range(rows)]
+    return float(np.median(us)), float(np.percentile(us, 10)), float(np.percentile(us, 90))
+
+
 def mechanism_row(rc, wk, key, budget_s=1.0):
-    """Resident (pipelined and synchronized) vs host round trip on one
-    workload; invocations as the workload defines them."""
+    """Resident (pipelined and synchronized), no-decision floor and host
+    round trip on one workload, invocations as the workload defines them.
+    Protocol: warmups, a calibration of the invocation count on the faster
+    (resident) mechanism, then MECH_ROWS timed rows per mechanism; the
+    median row is reported with its 10th-90th percentile spread."""
     import torch
     wl = wk.WORKLOADS[key]
     inp = wk.make_inputs(wl)
@@ -238,42 +276,48 @@ def mechanism_row(rc, wk, key, budget_s=1.0):
             per_inv = inp.n_sessions * T
         sets = Sets(rc, inp, T, 1 if wl.per_cohort_invocation else 2)
         stream = torch.cuda.current_stream().cuda_stream
-        # calibrate the invocation count on the faster (resident) mechanism
+        # warm up, then calibrate the invocations per row on the resident mechanism
         w, _ = time_resident(rc, h, sets, inp, T, 20, 5, stream, ranges)
-        n = int(max(20, min(20000, budget_s / 3 / max(w / 20, 1e-7))))
-        wall_r, _ = time_resident(rc, h, sets, inp, T, n, 5, stream, ranges)
+        n = int(max(10, min(20000, budget_s / 4 / MECH_ROWS / max(w / 20, 1e-7))))
+        r_med, r_lo, r_hi = _rows(lambda k: time_resident(rc, h, sets, inp, T, k, 0, stream, ranges)[0], n)
         rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_RESIDENT, *ranges[0], stream)
         res_counts = rc.rc_cohort_last_counts(h)
-        n_sync = max(10, n // 4)
-        wall_s = time_resident_synced(rc, h, sets, inp, T, n_sync, stream, ranges)
+        n_sync = max(5, n // 4)
+        s_med, s_lo, s_hi = _rows(lambda k: time_resident_synced(rc, h, sets, inp, T, k, stream, ranges),
+                                  n_sync)
         bits = floor_bits(rc, h, inp, T, stream)
-        wall_f = time_floor(rc, h, sets, bits, inp, T, n, 5, stream, ranges)
+        time_floor(rc, h, sets, bits, inp, T, 5, 5, stream, ranges)
+        f_med, f_lo, f_hi = _rows(lambda k: time_floor(rc, h, sets, bits, inp, T, k, 0, stream, ranges), n)
         w1 = time_hrt(rc, h, sets, inp, T, 3, 1, stream, ranges)
-        n_h = int(max(5, min(n, budget_s / 2 / max(w1 / 3, 1e-7))))
-        wall_h = time_hrt(rc, h, sets, inp, T, n_h, 0, stream, ranges)
+        n_h = int(max(3, min(n, budget_s / 4 / MECH_ROWS / max(w1 / 3, 1e-7))))
+        h_med, h_lo, h_hi = _rows(lambda k: time_hrt(rc, h, sets, inp, T, k, 0, stream, ranges), n_h)
         rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, *ranges[0], stream)
         hrt_counts = rc.rc_cohort_last_counts(h)
         torch.cuda.synchronize()
     finally:
         rc.rc_cohort_destroy(h)
-    us_r, us_s, us_h = wall_r / n * 1e6, wall_s / n_sync * 1e6, wall_h / n_h * 1e6
-    us_f = wall_f / n * 1e6
+    spread = lambda lo, hi: [round(lo, 3), round(hi, 3)]
     return {
         "workload": wl.title, "T": T, "transitions_per_invocation": per_inv,
-        "resident_us_per_invocation": round(us_r, 3),
-        "resident_us_per_chained_step": round(us_r / T, 4),
-        "resident_synced_us_per_invocation": round(us_s, 3),
-        "host_rt_us_per_invocation": round(us_h, 3),
-        "host_rt_us_per_chained_step": round(us_h / T, 4),
-        "host_over_resident": round(us_h / us_r, 3),
-        "host_over_resident_synced": round(us_h / us_s, 3),
-        "floor_us_per_invocation": round(us_f, 3),
-        "resident_over_floor": round(us_r / us_f, 3),
-        "resident_transitions_per_s": round(per_inv / (us_r * 1e-6), 1),
-        "host_rt_transitions_per_s": round(per_inv / (us_h * 1e-6), 1),
+        "resident_us_per_invocation": round(r_med, 3),
+        "resident_us_p10_p90": spread(r_lo, r_hi),
+        "resident_us_per_chained_step": round(r_med / T, 4),
+        "resident_synced_us_per_invocation": round(s_med, 3),
+        "resident_synced_us_p10_p90": spread(s_lo, s_hi),
+        "host_rt_us_per_invocation": round(h_med, 3),
+        "host_rt_us_p10_p90": spread(h_lo, h_hi),
+        "host_rt_us_per_chained_step": round(h_med / T, 4),
+        "host_over_resident": round(h_med / r_med, 3),
+        "host_over_resident_synced": round(h_med / s_med, 3),
+        "floor_us_per_invocation": round(f_med, 3),
+        "floor_us_p10_p90": spread(f_lo, f_hi),
+        "resident_over_floor": round(r_med / f_med, 3),
+        "resident_transitions_per_s": round(per_inv / (r_med * 1e-6), 1),
+        "host_rt_transitions_per_s": round(per_inv / (h_med * 1e-6), 1),
         "launches_per_invocation": {"resident": res_counts[0], "host_rt": hrt_counts[0]},
         "d2h_copies_per_invocation": {"resident": res_counts[1], "host_rt": hrt_counts[1]},
-        "invocations_timed": {"resident": n, "resident_synced": n_sync, "host_rt": n_h, "floor": n},
+        "invocations_per_row": {"resident": n, "resident_synced": n_sync, "host_rt": n_h, "floor": n},
+        "rows": MECH_ROWS,
     }
 
 
@@ -627,6 +671,15 @@ def main():
         },
         "verified_vs_oracle": verified,
     }
+    valu = stored_valu(wl.key)
+    if valu is not None:
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        busy = valu["insts_per_launch"] * 4.0 / (4 * cus * ENGINE_CLOCK_HZ * k_avg_ms * 1e-3)
+        out["valu"] = {"insts_per_launch": valu["insts_per_launch"],
+                       "insts_per_wave": round(valu["insts_per_launch"] / valu["waves"], 1),
+                       "busy_frac": round(busy, 4),
+                       "basis": "SQ_INSTS_VALU (committed rocprofv3 summary) x 4 cycles / "
+                                "(4 SIMDs x CUs x 2.4 GHz x measured kernel time)"}
     if not args.profile_only:
         hs = max(5, min(args.hrt_steps, args.steps))
         wall_h = time_hrt(rc, h, sets, inp, T, hs, 3, stream)
@@ -653,6 +706,11 @@ def main():
                 cpu["safe_suffix_k_r"] = safe_suffix_threshold(rc, wk)
             out["cpu_baseline"] = cpu
         out["hbm_measured"] = hbm_measured()
+        props = torch.cuda.get_device_properties(0)
+        out["device"] = {"name": props.name, "arch": getattr(props, "gcnArchName", None),
+                         "compute_units": props.multi_processor_count,
+                         "memory_GiB": round(props.total_memory / 2 ** 30, 1),
+                         "l2_cache_MiB": round(getattr(props, "L2_cache_size", 0) / 2 ** 20, 1)}
         if not args.no_former:
             # launch-to-start budget: the measured synchronized invocation of
             # a 256-session, 16-step batch when the K_r sweep ran, else 25 us
