@@ -6,14 +6,24 @@ workload.  One bench step is one device-resident chain over all sessions
 (every step of the hot path: route, decide, compact, update, emit, chain).
 It prints ONE JSON line with the contract fields plus:
 
+* ``roofline``: algorithmic bytes per launch of the resident chain kernel
+  over its average duration, timed with HIP events on the launch stream,
+  with the HBM traffic of the committed rocprofv3 counter summary;
+* ``valu``: VALU instructions per launch (committed SQ counter summary) and
+  the fraction of the chip's VALU issue they occupy;
 * ``host_roundtrip``: the same workload through the host-round-trip
   mechanism (4-byte readback + host branch + relaunch every chained step);
-* ``mechanisms``: resident vs host round trip on all five workloads
-  (microseconds per invocation and per chained step, launches and
-  device-to-host copies per invocation);
-* ``roofline``: algorithmic bytes per launch of the resident chain kernel
-  over its average duration, timed with HIP events on the launch stream;
-* ``cpu_baseline``: the single-threaded CPU oracle on the same workload.
+* ``floor``: the no-decision floor (decisions replayed from a bitmap);
+* ``mechanisms``: resident, synchronized resident, floor and host round trip
+  on all five workloads (median of timed rows: microseconds per invocation
+  and per chained step, launches and device-to-host copies per invocation);
+* ``cpu_baseline``: the single-threaded CPU oracle on the same workload, and
+  the safe-suffix threshold K_r (batch sizes and chain lengths where the
+  resident chain beats the oracle on one core and on all cores);
+* ``cohort_former``: the cohort shares F, P*, U, the online share A and
+  their ratios on seeded 1M-event arrival streams;
+* ``hbm_measured`` and ``device``: measured copy and fill bandwidth and the
+  device's properties, beside the spec peak.
 
 Inputs are synthetic and seeded (see paper_2608_12123_amd/workload.py).  The
 timed region rotates through enough buffer sets that the working set is
