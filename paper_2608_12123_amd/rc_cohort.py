@@ -23,6 +23,11 @@ LIB_PATH = os.path.join(PKG, "librc_cohort.so")
 RC_OK, RC_E_INVALID, RC_E_NOMEM, RC_E_DEVICE = 0, 1, 2, 3
 RC_ROUTE_MOD, RC_ROUTE_CDF = 0, 1
 RC_MODE_RESIDENT, RC_MODE_HOST_ROUNDTRIP = 0, 1
+# Shape limits of a descriptor (the #defines of rc_cohort.h).
+RC_MIN_WORDS, RC_MAX_WORDS = 4, 64
+RC_MAX_ROUTES = 1024
+RC_MAX_COHORT = 256
+RC_MAX_SESSIONS = 1 << 28
 
 EXPORTED = [
     "rc_cohort_create", "rc_cohort_step", "rc_cohort_run_chain", "rc_cohort_run_floor",

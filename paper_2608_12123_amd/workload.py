@@ -90,6 +90,18 @@ def uniform_unit(n: int, *keys: int, root: int = ROOT_SEED) -> np.ndarray:
     return (z >> np.uint64(11)).astype(np.float64) * (1.0 / (1 << 53))
 
 
+def device_uniform_u32(shape, *keys: int, device, root: int = ROOT_SEED):
+    """Uniform uint32 values, as int32 bit patterns, drawn on a torch device
+    by torch's seeded generator for that device (keyed like the host
+    streams).  For inputs too large to draw on the host; a test that checks
+    them copies the slices it needs to the host before they are used."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(stream_seed(*keys, root=root) & ((1 << 63) - 1))
+    return torch.randint(-(1 << 31), 1 << 31, tuple(shape), dtype=torch.int32, device=device,
+                         generator=g)
+
+
 # --------------------------------------------------------------------------
 # Derived route data and thresholds
 # --------------------------------------------------------------------------

@@ -31,6 +31,18 @@ def test_header_declares_the_boundary():
     assert sorted(rc.EXPORTED) == names
 
 
+def test_binding_limits_match_the_header():
+    text = open(HEADER).read()
+    defs = dict(re.findall(r"^#define\s+(RC_(?:MIN|MAX)_\w+)\s+\(?(\w+)", text, flags=re.M))
+    assert sorted(defs) == ["RC_MAX_COHORT", "RC_MAX_ROUTES", "RC_MAX_SESSIONS", "RC_MAX_WORDS",
+                            "RC_MIN_WORDS"]
+    shift = re.search(r"^#define\s+RC_MAX_SESSIONS\s+\(1u\s*<<\s*(\d+)\)", text, flags=re.M)
+    values = {k: int(v.rstrip("u")) for k, v in defs.items() if k != "RC_MAX_SESSIONS"}
+    values["RC_MAX_SESSIONS"] = 1 << int(shift.group(1))
+    for k, v in values.items():
+        assert getattr(rc, k) == v, k
+
+
 def test_library_exports_every_declared_symbol(lib):
     for name in declared_functions():
         assert hasattr(lib, name), name
