@@ -592,8 +592,9 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(cohorts are independent; see the sharding design). Run with --gpus 1.",
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(cohorts are independent, so sharding them over GPUs needs no "
+              "collective). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
