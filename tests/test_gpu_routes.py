@@ -1,4 +1,6 @@
-"""CDF route mode on degenerate threshold sets (needs an MI355X).
+"""Route keys at their boundaries (needs an MI355X).
+
+CDF mode on degenerate threshold sets, and MOD mode at multiples of R.
 
 The route is the number of thresholds at or below the outcome.  The kernels
 find it with a guide table and a fixed-trip binary search (the resident
@@ -88,3 +90,39 @@ def test_degenerate_cdf(orc, name, W):
             co.close()
         for k in KEYS:
             assert np.array_equal(got[k], want[k]), (name, W, label, k)
+
+
+def mod_boundary_outcomes(R):
+    top = (M32 // R) * R
+    vals = {0, 1, M32 - 1, M32, top, (top - 1) & M32, top + 1 if top < M32 else 0}
+    for k in (1, 2, 3, 1000, 65535, 1 << 20):
+        if k * R <= M32:
+            vals.update({k * R - 1, k * R, (k * R + 1) & M32})
+    return np.asarray(sorted(vals), dtype=np.uint32)
+
+
+@pytest.mark.parametrize("W", [8, 32, 64])
+@pytest.mark.parametrize("R", [1, 3, 7, 1000, 1023, 1024])
+def test_mod_boundaries(orc, R, W):
+    """MOD route mode, step-0 outcomes on and next to multiples of R and at
+    the top of the u32 range (power-of-two R takes the masked form)."""
+    sizes = [256, 64, 1, 31, 100, 256, 200, 7, 128] * 2
+    T, thr, step0 = 3, 32768, 0
+    inp = wk.make_custom(n_words=W, n_routes=R, route_mode=wk.ROUTE_MOD, decide_thr=thr,
+                         cohort_sizes=sizes, n_steps=T, seed_key=35_000 + W + R)
+    edges = mod_boundary_outcomes(R)
+    N = inp.n_sessions
+    pos = np.random.Generator(np.random.PCG64(35_001)).permutation(N)[:N // 4]
+    inp.outcome[pos] = np.resize(edges, pos.size)
+    say("mod R=%d W=%d C=%d N=%d boundary outcomes=%d" % (R, W, inp.n_cohorts, N, pos.size))
+    want = orc.run_inputs(inp, n_steps=T, step0=step0)
+    for label, mode in (("resident", rc.RC_MODE_RESIDENT),
+                        ("host round trip", rc.RC_MODE_HOST_ROUNDTRIP)):
+        co = rc.Cohort.from_inputs(inp, max_steps=T)
+        try:
+            co.run_chain(step0, T, mode)
+            got = co.download(T)
+        finally:
+            co.close()
+        for k in KEYS:
+            assert np.array_equal(got[k], want[k]), (R, W, label, k)
