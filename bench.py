@@ -614,7 +614,8 @@ def main():
     from paper_2608_12123_amd import rc_cohort as rc
     from paper_2608_12123_amd import workload as wk
 
-    assert torch.cuda.is_available(), "bench.py needs an MI355X"
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs an MI355X: no GPU is visible")
     rc.load_library()
     wl = wk.WORKLOADS[args.workload]
     inp = wk.make_inputs(wl)
