@@ -224,3 +224,34 @@ def test_invalid_buffers_rejected_untouched():
             assert np.array_equal(before[k], after[k]), k
     finally:
         co.close()
+
+
+def test_empty_calls_are_noops():
+    """n_steps == 0 or an empty cohort range: RC_OK, no launch, no copy, and
+    every buffer bit-unchanged, in both mechanisms, the floor and step()."""
+    import torch
+    inp = wk.make_custom(n_words=32, n_routes=64, route_mode=wk.ROUTE_CDF, decide_thr=19661,
+                         cohort_sizes=[256, 100, 31, 256], n_steps=2, seed_key=21,
+                         ld=643 + 9)
+    co = rc.Cohort.from_inputs(inp, max_steps=2)
+    try:
+        before = co.download(2)
+        bits = np.full((2, (co.ld + 31) // 32), 0xFFFFFFFF, dtype=np.uint32)
+        C = co.n_cohorts
+        for mode in (rc.RC_MODE_RESIDENT, rc.RC_MODE_HOST_ROUNDTRIP):
+            for T, cb, ce in ((0, 0, C), (2, 2, 2), (2, C, C), (0, 1, 1)):
+                assert co.run_chain(5, T, mode, cb, ce) == rc.RC_OK
+                assert co.last_counts() == (0, 0), (mode, T, cb, ce)
+        dbits = torch.from_numpy(bits.view(np.int32)).to(co.device)
+        for T, cb, ce in ((0, 0, C), (2, 3, 3)):
+            assert rc.rc_cohort_run_floor(co.handle, co.buffers, dbits.data_ptr(), T, cb,
+                                          ce) == rc.RC_OK
+            assert co.last_counts() == (0, 0)
+        assert co.step(0, 1, 1) == rc.RC_OK
+        assert co.last_counts() == (0, 0)
+        torch.cuda.synchronize()
+        after = co.download(2)
+        for k in before:
+            assert np.array_equal(before[k], after[k]), k
+    finally:
+        co.close()
