@@ -72,6 +72,7 @@
 #include "rc_cohort.h"
 
 
+
 namespace {
 
 // ---------------------------------------------------------------------------
@@ -788,10 +789,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 // Rows of the mask image are W + 4 words apart (one zero block of padding
 // shifts consecutive rows across the LDS banks), so block q of a row is an
 // immediate offset from the row's byte offset.
+// PIPED (W = 32): the A lanes keep only the chain and run it one 4-step
+// chunk ahead; the B lanes replay every word and emit the effects (see PIPE
+// below).
 // FLOOR: the no-decision floor -- the A lanes read every decision from the
 // bitmap instead of computing it (SPLIT: the first two chunks' words loaded
 // after the first barrier, later chunks' a chunk ahead).
-template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT, bool FLOOR>
+template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT, bool FLOOR, bool PIPED>
 struct ChainF {
     // Effect stores stay on the normal path: cohorts spanning wavefronts
     // fill each line from several wavefronts.
@@ -804,12 +808,23 @@ struct ChainF {
     // waiting for everything on the vector-memory counter, so a lane that
     // emits effects should have no load left to wait for -- and the 28 words
     // of the B lanes then arrive while the effects go out.
-    static constexpr int WA = SPLIT ? (WMAX == 32 ? 4 : WMAX / 2) : WMAX;
+    // PIPE (PIPED, SPLIT at WMAX = 32): the A lanes hold only word 0 and
+    // the outcome and run the chain one 4-step chunk ahead, storing nothing
+    // but the final outcome; the B lanes hold all the words, replay each
+    // chunk behind it and emit the effects.  The chain of chunk k + 1 then
+    // overlaps the replay of chunk k, where the two-role split runs its
+    // 16-step chunks' chains and replays in turn.  The B lanes carry more
+    // work per step, so this pays only for chains longer than one 16-step
+    // chunk in launches of at most one workgroup per CU (the host decides).
+    static constexpr bool PIPE = SPLIT && WMAX == 32 && PIPED;
+    static constexpr int WA = PIPE ? 0 : SPLIT ? (WMAX == 32 ? 4 : WMAX / 2) : WMAX;
     static constexpr int WB = SPLIT ? WMAX - WA : 0;
     static constexpr int WS = WA > WB ? WA : WB;  // state registers per lane
     static constexpr int NBA = WA / 4, NBB = WB / 4;  // 16-byte blocks per lane
     static constexpr uint32_t RS = (WMAX + 4) * 4;       // row stride in bytes
-    static constexpr int TC = WMAX <= 32 ? 16 : 8;       // steps per chunk
+    // steps per chunk (PIPE: two chunks in flight, each in its own half of
+    // the 16-step control and count areas)
+    static constexpr int TC = PIPE ? 4 : WMAX <= 32 ? 16 : 8;
     static constexpr uint32_t WG = (SPLIT ? 2 : 1) * NWAVE * 64;
     static constexpr int SB = WMAX <= 32 ? (SPLIT ? 5 : 10) : (SPLIT ? 3 : 6);
 
@@ -829,8 +844,12 @@ struct ChainF {
         const uint32_t W = a.n_words;
         const uint32_t R = a.ra.n_routes;
         const uint32_t T = a.n_steps;
-        uint32_t* lds_cnt = lds + a.img_words;          // [TC][NWAVE + 4]
-        uint32_t* lds_x = lds_cnt + TC * CNT_STRIDE;    // SPLIT: [TC][2][NWAVE * 64]
+        // The host reserves 16 steps of each: counts [16][NWAVE + 4], then
+        // (SPLIT) the control handed to the B lanes, [16][2][NWAVE * 64].
+        // PIPE uses the first 2 TC steps of both (two chunks in flight).
+        static_assert(TC <= 16 && (!PIPE || 2 * TC <= 16), "LDS control and count areas hold 16 steps");
+        uint32_t* lds_cnt = lds + a.img_words;
+        uint32_t* lds_x = lds_cnt + 16 * CNT_STRIDE;
         const uint32_t* lds_tools = lds + a.tools_off;
 
         const uint32_t* lds_rows = lds + a.rows_off;
@@ -963,6 +982,11 @@ struct ChainF {
         // control.  Chunk 0's chain runs ahead of the chunk loop, so that no
         // wait for the state words still in flight is placed before it.
         uint32_t ctl[TC], add[TC];
+        // PIPE: first step slot of the half of the control and count areas
+        // that holds the chunk starting at t0 (chunks alternate halves)
+        auto half_of = [&](uint32_t t0) -> uint32_t {
+            return PIPE ? ((t0 / (uint32_t)TC) & 1u) * (uint32_t)TC : 0u;
+        };
         auto chain_chunk = [&](uint32_t t0) {
             const uint32_t n = (T - t0) < (uint32_t)TC ? (T - t0) : (uint32_t)TC;
 #pragma unroll
@@ -1021,17 +1045,18 @@ struct ChainF {
                 }
                 // counts of the chunk's steps: every lane writes the same
                 // (uniform) value to the same address, so no lane mask
+                const uint32_t par = half_of(t0);
                 if constexpr (MULTI) {
 #pragma unroll
                     for (int i = 0; i < TC; ++i)
-                        lds_cnt[i * CNT_STRIDE + wa] = (uint32_t)__popcll(__ballot((ctl[i] >> 5) & 1u));
+                        lds_cnt[(par + i) * CNT_STRIDE + wa] = (uint32_t)__popcll(__ballot((ctl[i] >> 5) & 1u));
                 }
                 // the control for the B lanes
                 if constexpr (SPLIT) {
 #pragma unroll
                     for (int i = 0; i < TC; ++i) {
-                        lds_x[(2 * i) * (NWAVE * 64) + alane] = ctl[i];
-                        lds_x[(2 * i + 1) * (NWAVE * 64) + alane] = add[i];
+                        lds_x[(2 * (par + i)) * (NWAVE * 64) + alane] = ctl[i];
+                        lds_x[(2 * (par + i) + 1) * (NWAVE * 64) + alane] = add[i];
                     }
                 }
                 __builtin_amdgcn_s_setprio(0);
@@ -1039,22 +1064,22 @@ struct ChainF {
         };
 
         // Replay of the chunk starting at t0 over this lane's 16-byte word
-        // blocks [QLO, QHI), with (EFF, A lanes) the slots and effects, step
-        // by step.  The LDS reads of step i + 1 (mask blocks and, with EFF,
-        // counts and tool pair) are issued before step i is computed; past
-        // the chunk's last step they read the zero row (valid addresses,
-        // values unused).  The step count is re-read so that no per-step
-        // condition stays live across the phases.
+        // blocks [QLO, QHI), with (EFF: the A lanes, or the B lanes under
+        // PIPE) the slots and effects, step by step.  PREF: the LDS reads of
+        // step i + 1 (mask blocks and, with EFF, counts and tool pair) are
+        // issued before step i is computed; past the chunk's last step they
+        // read the zero row (valid addresses, values unused).  The step count
+        // is re-read so that no per-step condition stays live across the
+        // phases.
         auto replay = [&](uint32_t t0, auto qlo_c, auto qhi_c, auto eff_c, auto pref_c) {
             constexpr int QLO = decltype(qlo_c)::value;
             constexpr int QHI = decltype(qhi_c)::value;
             constexpr int NQ = QHI - QLO;
             constexpr bool EFF = decltype(eff_c)::value;
             constexpr bool PREF = decltype(pref_c)::value;
-            static_assert(PREF || !EFF, "the effect pass prefetches");
             const uint32_t n = (T - t0) < (uint32_t)TC ? (T - t0) : (uint32_t)TC;
             const uint32_t nr = opaque_s(n);
-            const uint32_t* cq0 = lds_cnt + (L.flags >> 24);
+            const uint32_t* cq0 = lds_cnt + (L.flags >> 24) + half_of(t0) * CNT_STRIDE;
             const uint32_t qoff = (wbase + 4u * QLO) * 4u;  // byte offset of the first block in a row
             uint4 mc[NQ];
             uint32_t cc[4] = {0u, 0u, 0u, 0u}, tpc = 0u;
@@ -1078,6 +1103,11 @@ struct ChainF {
                     const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
 #pragma unroll
                     for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds_rows, rowoff + 16u * q);
+                    if constexpr (EFF) {
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[i * CNT_STRIDE + k] : 0u;
+                        tpc = lds_tools[c >> 6];
+                    }
                 }
                 if (PREF && i + 1 < TC) {
                     const uint32_t c = ctl[i + 1];
@@ -1180,7 +1210,56 @@ struct ChainF {
         // one role's accesses at a time.  Chunk 0 runs outside the chunk
         // loop: the compiler flushes every outstanding vector-memory access
         // in the preheader of a loop that stores without loading.
-        if constexpr (SPLIT) {
+        if constexpr (PIPE) {
+            // The same barriers in both roles: a bare one after staging, then
+            // one per chunk.  Barrier k + 1 publishes chunk k's control and
+            // counts (A) and closes the replay of chunk k - 1 (B); chunk k + 2
+            // reuses chunk k's half only after barrier k + 2, when its replay
+            // is done.
+            if (!role_b) {
+                stage_a();
+                bare_barrier();
+                load_db();
+                uint32_t db1[TC];
+                if constexpr (FLOOR) {
+#pragma unroll
+                    for (int i = 0; i < TC; ++i)
+                        db1[i] = (uint32_t)(TC + i) < T ? dword_of(a, (uint32_t)(TC + i), L.active ? L.s : 0u) : 0u;
+                    dm = pack(db);
+                    dm1 = pack(db1);
+                }
+                for (uint32_t t0 = 0; t0 < T; t0 += TC) {
+                    chain_chunk(t0);
+                    lds_barrier();
+                }
+                if (L.active) st32<true>(a.outcome, soff, o);
+            } else {
+                stage_b();
+                bare_barrier();
+                load_words(std::integral_constant<int, WB>{});
+                // the row loads issued before the WB state loads have landed
+                // (with W < WMAX fewer state loads were issued: wait for all)
+                wait_vmcnt<EXACT ? WB : 0>();
+                lds_barrier();
+                auto read_ctl = [&](uint32_t t0) {
+                    const uint32_t par = half_of(t0);
+#pragma unroll
+                    for (int i = 0; i < TC; ++i) {
+                        ctl[i] = lds_x[(2 * (par + i)) * (NWAVE * 64) + alane];
+                        add[i] = lds_x[(2 * (par + i) + 1) * (NWAVE * 64) + alane];
+                    }
+                };
+                read_ctl(0u);
+                wait_vmcnt<0>();  // every word is needed at the first step
+                replay(0u, Z{}, NB{}, Yes{}, No{});
+                for (uint32_t t0 = TC; t0 < T; t0 += TC) {
+                    lds_barrier();
+                    read_ctl(t0);
+                    replay(t0, Z{}, NB{}, Yes{}, No{});
+                }
+                store_state(std::integral_constant<int, WB>{}, false);
+            }
+        } else if constexpr (SPLIT) {
             if (!role_b) {
                 stage_a();
                 bare_barrier();
@@ -1262,16 +1341,16 @@ struct ChainF {
 // full-image chain at W <= 32 run two 512-lane workgroups per CU, so they are
 // held to four wavefronts per SIMD (at most 128 VGPRs).  At W = 64 the
 // two-lane full-image chain needs more registers and runs one per CU.
-template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool FLOOR>
+template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool FLOOR, bool PIPED>
 __global__ __launch_bounds__((FULL && WMAX >= 32 ? 2 : 1) * NWAVE * 64, (!FULL || WMAX == 32) ? 4 : 1)
 void rc_chain_kernel(ChainArgs a) {
     extern __shared__ uint4 lds4[];
     if constexpr (FULL) {
         constexpr bool SPLIT = WMAX >= 32;
         if (blockIdx.x < a.bins_a_n)
-            ChainF<WMAX, EXACT, NWAVE, RK, false, SPLIT, FLOOR>::run(a, a.bins_a_lo + blockIdx.x, lds4);
+            ChainF<WMAX, EXACT, NWAVE, RK, false, SPLIT, FLOOR, PIPED>::run(a, a.bins_a_lo + blockIdx.x, lds4);
         else
-            ChainF<WMAX, EXACT, NWAVE, RK, true, SPLIT, FLOOR>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
+            ChainF<WMAX, EXACT, NWAVE, RK, true, SPLIT, FLOOR, PIPED>::run(a, a.bins_b_lo + (blockIdx.x - a.bins_a_n), lds4);
     } else {
         if (blockIdx.x < a.bins_a_n)
             Chain<WMAX, EXACT, NWAVE, FULL, RK, false, FLOOR>::run(a, a.bins_a_lo + blockIdx.x, lds4);
@@ -1402,35 +1481,49 @@ typedef void (*ChainFn)(ChainArgs);
 typedef void (*DecideFn)(DecideArgs);
 typedef void (*BodyFn)(BodyArgs);
 
+// The pipelined split exists for the full image at WMAX = 32 only.
+bool has_piped(uint32_t wmax, bool full) { return full && wmax == 32u; }
+
 template <int WMAX, bool EXACT, int RK, bool FLOOR>
-ChainFn chain_fn(bool full) {
+ChainFn chain_fn(bool full, bool piped) {
     if (!full) {
-        if constexpr (WMAX >= 32) return rc_chain_kernel<WMAX, EXACT, 8, false, RK, FLOOR>;
+        if constexpr (WMAX >= 32) return rc_chain_kernel<WMAX, EXACT, 8, false, RK, FLOOR, false>;
         return nullptr;
     }
-    return rc_chain_kernel<WMAX, EXACT, 4, true, RK, FLOOR>;
+    if constexpr (WMAX == 32)
+        if (piped) return rc_chain_kernel<WMAX, EXACT, 4, true, RK, FLOOR, true>;
+    return rc_chain_kernel<WMAX, EXACT, 4, true, RK, FLOOR, false>;
 }
 
 template <int WMAX, bool EXACT, bool FLOOR>
-ChainFn chain_fn_rk(bool full, int rk) {
-    return rk == RK_POW2 ? chain_fn<WMAX, EXACT, RK_POW2, FLOOR>(full)
-         : rk == RK_MOD ? chain_fn<WMAX, EXACT, RK_MOD, FLOOR>(full)
-                        : chain_fn<WMAX, EXACT, RK_CDF, FLOOR>(full);
+ChainFn chain_fn_rk(bool full, bool piped, int rk) {
+    return rk == RK_POW2 ? chain_fn<WMAX, EXACT, RK_POW2, FLOOR>(full, piped)
+         : rk == RK_MOD ? chain_fn<WMAX, EXACT, RK_MOD, FLOOR>(full, piped)
+                        : chain_fn<WMAX, EXACT, RK_CDF, FLOOR>(full, piped);
 }
 
 template <bool FLOOR>
-ChainFn pick_chain_t(uint32_t wmax, bool exact, bool full, int rk) {
+ChainFn pick_chain_t(uint32_t wmax, bool exact, bool full, bool piped, int rk) {
     switch (wmax) {
-        case 4: return exact ? chain_fn_rk<4, true, FLOOR>(full, rk) : chain_fn_rk<4, false, FLOOR>(full, rk);
-        case 8: return exact ? chain_fn_rk<8, true, FLOOR>(full, rk) : chain_fn_rk<8, false, FLOOR>(full, rk);
-        case 16: return exact ? chain_fn_rk<16, true, FLOOR>(full, rk) : chain_fn_rk<16, false, FLOOR>(full, rk);
-        case 32: return exact ? chain_fn_rk<32, true, FLOOR>(full, rk) : chain_fn_rk<32, false, FLOOR>(full, rk);
-        default: return exact ? chain_fn_rk<64, true, FLOOR>(full, rk) : chain_fn_rk<64, false, FLOOR>(full, rk);
+        case 4: return exact ? chain_fn_rk<4, true, FLOOR>(full, piped, rk) : chain_fn_rk<4, false, FLOOR>(full, piped, rk);
+        case 8: return exact ? chain_fn_rk<8, true, FLOOR>(full, piped, rk) : chain_fn_rk<8, false, FLOOR>(full, piped, rk);
+        case 16: return exact ? chain_fn_rk<16, true, FLOOR>(full, piped, rk) : chain_fn_rk<16, false, FLOOR>(full, piped, rk);
+        case 32: return exact ? chain_fn_rk<32, true, FLOOR>(full, piped, rk) : chain_fn_rk<32, false, FLOOR>(full, piped, rk);
+        default: return exact ? chain_fn_rk<64, true, FLOOR>(full, piped, rk) : chain_fn_rk<64, false, FLOOR>(full, piped, rk);
     }
 }
 
-ChainFn pick_chain(uint32_t wmax, bool exact, bool full, int rk, bool floor) {
-    return floor ? pick_chain_t<true>(wmax, exact, full, rk) : pick_chain_t<false>(wmax, exact, full, rk);
+ChainFn pick_chain(uint32_t wmax, bool exact, bool full, bool piped, int rk, bool floor) {
+    return floor ? pick_chain_t<true>(wmax, exact, full, piped, rk)
+                 : pick_chain_t<false>(wmax, exact, full, piped, rk);
+}
+
+// The pipelined split for a launch: chains longer than one 16-step chunk,
+// at most one workgroup per CU.  Measured on MI355X (256-session cohorts,
+// W = 32): 6-10% faster than the two-role split from 1 to 256 workgroups at
+// T = 32, slower beyond that and at every size for T <= 16.
+bool use_piped(uint32_t wmax, bool full, uint32_t T, uint32_t grid) {
+    return has_piped(wmax, full) && T > 16u && grid <= 256u;
 }
 
 template <int WMAX, bool EXACT>
@@ -1807,7 +1900,8 @@ int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
     a.dbits = dbits;
     a.dwords = (b->ld + 31u) / 32u;
     const uint32_t grid = a.bins_a_n + a.bins_b_n;  // one workgroup per bin
-    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind, dbits != nullptr);
+    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, use_piped(h->wmax, h->full, T, grid),
+                            h->route_kind, dbits != nullptr);
     hipLaunchKernelGGL(fn, dim3(grid), dim3(h->chain_threads), h->chain_lds_bytes, stream, a);
     if (launch_ok() != RC_OK) return RC_E_DEVICE;
     h->last_launches = 1;
@@ -2028,8 +2122,10 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
         h->ra.guide_top = 0;
         while (span && (h->ra.guide_top << 1) <= span) h->ra.guide_top = h->ra.guide_top ? h->ra.guide_top << 1 : 1u;
     }
-    for (int fl = 0; fl < 2 && rc == RC_OK; ++fl) {
-        ChainFn fn = pick_chain(h->wmax, h->exact, h->full, h->route_kind, fl != 0);
+    for (int v = 0; v < 4 && rc == RC_OK; ++v) {
+        const bool fl = (v & 1) != 0, piped = (v & 2) != 0;
+        if (piped && !has_piped(h->wmax, h->full)) continue;
+        ChainFn fn = pick_chain(h->wmax, h->exact, h->full, piped, h->route_kind, fl);
         if (!fn) rc = RC_E_DEVICE;
         if (rc == RC_OK && hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                                (int)h->chain_lds_bytes) != hipSuccess) rc = RC_E_DEVICE;

@@ -167,8 +167,8 @@ def test_resident_matches_host_roundtrip_and_is_deterministic():
     for mode in (rc.RC_MODE_RESIDENT, rc.RC_MODE_RESIDENT, rc.RC_MODE_HOST_ROUNDTRIP):
         outs.append(gpu_run_ranges(inp, 16, mode, [(0, inp.n_cohorts)]))
     for k in outs[0]:
-        assert outs[0][k].tobytes() == outs[1][k].tobytes(), k
-        assert outs[0][k].tobytes() == outs[2][k].tobytes(), k
+        assert np.array_equal(outs[0][k], outs[1][k]), ("resident run twice", k)
+        assert np.array_equal(outs[0][k], outs[2][k]), ("resident vs host round trip", k)
 
 
 def test_launch_and_copy_counts():
@@ -255,3 +255,20 @@ def test_empty_calls_are_noops():
             assert np.array_equal(before[k], after[k]), k
     finally:
         co.close()
+
+
+@pytest.mark.parametrize("mode", sorted(MODES))
+def test_both_two_lane_kernels(orc, mode):
+    """W = 32, T = 32: one launch of 1,000 cohorts (more workgroups than CUs:
+    the two-role split, two 16-step chunks) and the same cohorts in launches
+    of 1, 100 and 256 (the pipelined split, eight 4-step chunks)."""
+    wl = wk.WORKLOADS["k256"]
+    inp = wk.make_inputs(wl, chunk=1)
+    C, T = inp.n_cohorts, wl.n_steps
+    say("both two-lane kernels mode=%s C=%d T=%d" % (mode, C, T))
+    want = oracle_run(orc, inp, T, step0=3)
+    whole = gpu_run_ranges(inp, T, MODES[mode], [(0, C)], step0=3)
+    assert_same(whole, want, "one launch")
+    cuts = [0, 1, 101, 357, 613, 869, C]
+    pieces = gpu_run_ranges(inp, T, MODES[mode], list(zip(cuts[:-1], cuts[1:])), step0=3)
+    assert_same(pieces, want, "launches of 1 to 256 cohorts")
