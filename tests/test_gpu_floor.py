@@ -146,3 +146,20 @@ def test_floor_invalid_arguments_touch_nothing():
             assert np.array_equal(before[k], after[k]), k
     finally:
         co.close()
+
+
+def test_floor_both_two_lane_kernels(orc):
+    """W = 32, T = 32 with the oracle's recorded decisions: one launch of
+    1,000 cohorts (the two-role split, two 16-step chunks) and launches of at
+    most 256 cohorts (the pipelined split, 4-step chunks) reproduce the
+    oracle's chain."""
+    wl = wk.WORKLOADS["k256"]
+    inp = wk.make_inputs(wl, chunk=2)
+    C, T = inp.n_cohorts, wl.n_steps
+    say("floor, both two-lane kernels: C=%d T=%d" % (C, T))
+    want = orc.run_inputs(inp, n_steps=T, record=True)
+    whole = gpu_floor(inp, want["decisions"], T, [(0, C)])
+    assert_same(whole, want, "one launch")
+    cuts = [0, 256, 257, 513, 769, C]
+    pieces = gpu_floor(inp, want["decisions"], T, list(zip(cuts[:-1], cuts[1:])))
+    assert_same(pieces, want, "launches of at most 256 cohorts")
