@@ -504,7 +504,7 @@ __device__ __forceinline__ void band0(uint32_t (&S)[WMAX], const uint32_t (&tv)[
     if constexpr (J < 16) {
         M[J] = mul_small<J + 1>(tv[J]);
         if constexpr (J < WMAX)
-            if (EXACT || (uint32_t)J < W) S[J] = (rotr32(S[J], sh) ^ M[J]) + oo;
+            S[J] = (rotr32(S[J], sh) ^ M[J]) + oo;  // words >= W: padding, see band()
         band0<J + 1, EXACT, WMAX>(S, tv, M, sh, oo, W);
     }
 }
@@ -521,7 +521,10 @@ __device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[1
         // one v_lshl_add_u32 per mask (written out, so that the shift is
         // not computed once and kept for every band)
         M[j] = after_word(lshl4_add(tv[j], M[j]), S[base + j - 16]);
-        if (EXACT || (uint32_t)(base + j) < W) S[base + j] = (rotr32(S[base + j], sh) ^ M[j]) + oo;
+        // Every word is updated, also past W: those registers start at zero,
+        // are never stored, and feed nothing else, while a per-word branch
+        // here would keep extra values live across the bands (and spill).
+        S[base + j] = (rotr32(S[base + j], sh) ^ M[j]) + oo;
     }
 }
 
