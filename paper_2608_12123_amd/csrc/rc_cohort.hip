@@ -468,6 +468,20 @@ __device__ __forceinline__ uint32_t dword_of(const ChainArgs& a, uint32_t t, uin
     return a.dbits[(size_t)t * a.dwords + (s >> 5)];
 }
 
+// No-decision floor, table image: session s's decisions of the 16 steps from
+// t0 (bit i = step t0 + i; steps past the chain read its last step's word),
+// zero for idle lanes.  One word at a time, on purpose (see the caller).
+__device__ __forceinline__ uint32_t decision_block(const ChainArgs& a, const LaneCohort& L, uint32_t t0) {
+    const uint32_t s = L.active ? L.s : 0u;
+    uint32_t m = 0u;
+#pragma unroll 1
+    for (uint32_t i = 0; i < 16u; ++i) {
+        const uint32_t t = t0 + i < a.n_steps ? t0 + i : a.n_steps - 1u;
+        m |= ((dword_of(a, t, s) >> (s & 31u)) & 1u) << i;
+    }
+    return L.active ? m : 0u;
+}
+
 // One row (WM words) of the image; logical block q of row r sits at block
 // q ^ (r mod NB), so its byte address is one XOR away.
 template <int WM>
@@ -547,7 +561,7 @@ struct Chain {
     struct Lane {
         uint32_t S[WMAX];
         uint32_t o, r, step, pub;
-        uint32_t dw;  // FLOOR: bitmap word of the next step to decide
+        uint32_t dm;  // FLOOR: this lane's decisions of the current 16-step block (bit i)
         bool dk;
         uint64_t bal;
         uint32_t c4[4];
@@ -589,8 +603,12 @@ struct Chain {
         const uint32_t r_n = route_of<RK>(o_n, a.ra, lds + a.cdf_off, lds + a.guide_off);
         bool d_n;
         if constexpr (FLOOR) {
-            d_n = L.active && ((st.dw >> (L.s & 31u)) & 1u);
-            if (t + 2u < a.n_steps) st.dw = dword_of(a, t + 2u, L.active ? L.s : 0u);
+            // a new 16-step block: its words, one at a time (a wait for a
+            // load drains the effect stores in flight, so it happens once
+            // per block, and the serial loop keeps no extra registers live)
+            const uint32_t tn = t + 1u;
+            if ((tn & 15u) == 0u && tn < a.n_steps) st.dm = decision_block(a, L, tn);
+            d_n = L.active && ((st.dm >> (tn & 15u)) & 1u);
         } else {
             d_n = L.active && ((dev_fmix32(st.S[0] ^ o_n ^ (st.step + 1u)) & 0xFFFFu) < a.thr);
         }
@@ -702,13 +720,15 @@ struct Chain {
 #pragma unroll
         for (int w = 0; w < WMAX; ++w) st.S[w] = 0;
         st.o = 0;
-        uint32_t dw0 = 0u;
-        st.dw = 0u;
+        // FLOOR: the first 16 steps' decision words, issued ahead of the
+        // state words (steps past the chain read its last step's word), so
+        // that the loop has no global load until step 16
+        uint32_t dwd[16];
+        st.dm = 0u;
         if constexpr (FLOOR) {
-            // the first two steps' decision words, ahead of the state words
             const uint32_t ls = L.active ? L.s : 0u;
-            dw0 = dword_of(a, 0u, ls);
-            if (T > 1u) st.dw = dword_of(a, 1u, ls);
+#pragma unroll
+            for (uint32_t i = 0; i < 16u; ++i) dwd[i] = dword_of(a, i < T ? i : T - 1u, ls);
         }
         if (L.active) {
             const uint32_t ldw = opaque_s(a.ld);
@@ -717,12 +737,18 @@ struct Chain {
             for (int w = 0; w < WMAX; ++w)
                 if (EXACT || (uint32_t)w < W) st.S[w] = ld32(a.state + (size_t)w * ldw, soff);
         }
+        if constexpr (FLOOR) {
+            uint32_t m = 0u;
+#pragma unroll
+            for (uint32_t i = 0; i < 16u; ++i) m |= ((dwd[i] >> (L.s & 31u)) & 1u) << i;
+            st.dm = L.active ? m : 0u;
+        }
 
         // decision of the first step
         st.step = a.step0;
         st.r = route_of<RK>(st.o, a.ra, lds + a.cdf_off, lds + a.guide_off);
         if constexpr (FLOOR)
-            st.dk = L.active && ((dw0 >> (L.s & 31u)) & 1u);
+            st.dk = (st.dm & 1u) != 0u;
         else
             st.dk = L.active && ((dev_fmix32(st.S[0] ^ st.o ^ st.step) & 0xFFFFu) < a.thr);
         st.bal = __ballot(st.dk);
@@ -872,9 +898,10 @@ struct ChainF {
         // loaded with the outcome before the first barrier, apart from the
         // state words that follow it.
         uint32_t s0 = 0u;
-        uint32_t db[TC];  // FLOOR: the decision words of the first chunk (A lanes)
+        uint32_t db[TC];   // FLOOR: the decision words of the first chunk (A lanes)
+        uint32_t db1[TC];  // FLOOR, SPLIT: those of the second chunk
 #pragma unroll
-        for (int i = 0; i < TC; ++i) db[i] = 0u;
+        for (int i = 0; i < TC; ++i) db[i] = db1[i] = 0u;
 #pragma unroll
         for (int w = 0; w < WS; ++w) S[w] = 0u;
         // FLOOR: a chunk's decisions packed into one register (bit i = step
@@ -914,7 +941,25 @@ struct ChainF {
             }
             o = ld32(a.outcome, loff);
             s0 = ld32(a.state, loff);
-            __builtin_amdgcn_s_waitcnt(0);  // chain section in LDS, outcome and word 0 in VGPRs
+            if constexpr (FLOOR) {
+                // The decision words of the first two chunks go out right
+                // behind them, so that their latency overlaps the staging.
+                // Steps past the chain read its last step's word: exactly
+                // 2 TC loads follow, and waiting until at most that many are
+                // outstanding completes everything issued before them (loads
+                // retire in order).  They are packed before any store.
+                asm volatile("" ::: "memory");
+                const uint32_t ls = L.active ? L.s : 0u;
+#pragma unroll
+                for (int i = 0; i < TC; ++i) db[i] = dword_of(a, (uint32_t)i < T ? (uint32_t)i : T - 1u, ls);
+#pragma unroll
+                for (int i = 0; i < TC; ++i)
+                    db1[i] = dword_of(a, (uint32_t)(TC + i) < T ? (uint32_t)(TC + i) : T - 1u, ls);
+                asm volatile("" ::: "memory");
+                wait_vmcnt<2 * TC>();  // chain section in LDS, outcome and word 0 in VGPRs
+            } else {
+                __builtin_amdgcn_s_waitcnt(0);  // chain section in LDS, outcome and word 0 in VGPRs
+            }
         };
         auto stage_b = [&]() {
             const uint32_t c4 = a.chain_words / 4u;
@@ -1222,12 +1267,7 @@ struct ChainF {
             if (!role_b) {
                 stage_a();
                 bare_barrier();
-                load_db();
-                uint32_t db1[TC];
                 if constexpr (FLOOR) {
-#pragma unroll
-                    for (int i = 0; i < TC; ++i)
-                        db1[i] = (uint32_t)(TC + i) < T ? dword_of(a, (uint32_t)(TC + i), L.active ? L.s : 0u) : 0u;
                     dm = pack(db);
                     dm1 = pack(db1);
                 }
@@ -1266,18 +1306,9 @@ struct ChainF {
             if (!role_b) {
                 stage_a();
                 bare_barrier();
-                // FLOOR: the decision words of the first two chunks go out
-                // after the barrier (so that the other wavefronts are not held
-                // at it while they arrive) and are packed before any store is
-                // issued: once stores are outstanding, waiting for a load
-                // drains them too.
-                load_db();
-                uint32_t db1[TC];
-                if constexpr (FLOOR) {
-#pragma unroll
-                    for (int i = 0; i < TC; ++i)
-                        db1[i] = (uint32_t)(TC + i) < T ? dword_of(a, (uint32_t)(TC + i), L.active ? L.s : 0u) : 0u;
-                }
+                // FLOOR: the decision words of the first two chunks (issued in
+                // stage_a) are packed before any store is issued: once stores
+                // are outstanding, waiting for a load drains them too.
                 load_words(std::integral_constant<int, WA>{});
                 if constexpr (FLOOR) {
                     dm = pack(db);
