@@ -547,7 +547,8 @@ __device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[1
 // exchanges popcounts behind a workgroup barrier; otherwise every cohort lies
 // inside one wavefront and no barrier is needed.
 // FLOOR: the no-decision floor -- every decision is read from the bitmap
-// (prefetched a step ahead) instead of computed; nothing else changes.
+// (16 steps of a lane's decisions loaded at once and packed into one
+// register) instead of computed; nothing else changes.
 template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool MULTI, bool FLOOR>
 struct Chain {
     static constexpr int MW = FULL ? WMAX : 16;
@@ -822,8 +823,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 // chunk ahead; the B lanes replay every word and emit the effects (see PIPE
 // below).
 // FLOOR: the no-decision floor -- the A lanes read every decision from the
-// bitmap instead of computing it (SPLIT: the first two chunks' words loaded
-// after the first barrier, later chunks' a chunk ahead).
+// bitmap instead of computing it (SPLIT: the first two chunks' words issued
+// with the staging loads, later chunks' a chunk ahead).
 template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT, bool FLOOR, bool PIPED>
 struct ChainF {
     // Effect stores stay on the normal path: cohorts spanning wavefronts
@@ -925,8 +926,9 @@ struct ChainF {
 
         // (a1, a2) Staging.  SPLIT, A wavefronts: only what the word-0 chain
         // reads -- the chain section of the image (word-0 masks, CDF
-        // thresholds, guide table), the outcome and word 0 -- so that the
-        // chain starts after the first barrier.  SPLIT, B wavefronts (idle
+        // thresholds, guide table), the outcome and word 0 (FLOOR: and the
+        // first two chunks' decision words) -- so that the chain starts
+        // after the first barrier.  SPLIT, B wavefronts (idle
         // until the chunk's control is published): the mask rows and tool
         // pairs, with direct-to-LDS loads that stay in flight across the
         // first (bare) barrier; every B lane waits for its own before the
