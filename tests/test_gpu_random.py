@@ -81,3 +81,47 @@ def test_random_shape(orc, case):
         finally:
             co.close()
         assert_same(got, want, "case %d %s" % (case, label))
+
+
+def draw_two_lane(case):
+    """Shapes of the pipelined two-lane kernel: W 17..32, a route count whose
+    full mask image fits, T > 16, launches of at most 256 cohorts."""
+    rng = np.random.Generator(np.random.PCG64(92_000 + case))
+    W = int(rng.integers(17, 33))
+    R = int(rng.choice([1, 3, 16, 64, 200, 256, 400]))
+    mode = wk.ROUTE_CDF if (R > 1 and rng.random() < 0.5) else wk.ROUTE_MOD
+    thr = int(rng.choice([0, 3277, 19661, 32768, 65536]))
+    mixes = ([256], [1, 31, 32, 33, 64, 65, 100, 255, 256], list(range(1, 257)))
+    kinds = mixes[int(rng.integers(0, len(mixes)))]
+    sizes = [int(x) for x in rng.choice(kinds, size=int(rng.integers(1, 60)))]
+    T = int(rng.choice([17, 20, 31, 32, 33, 48]))
+    pad = int(rng.choice([0, 5]))
+    step0 = int(rng.choice([0, 0xFFFFFFF8]))
+    return W, R, mode, thr, sizes, T, pad, step0
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_two_lane_long_chain(orc, case):
+    W, R, mode, thr, sizes, T, pad, step0 = draw_two_lane(case)
+    N = sum(sizes)
+    inp = wk.make_custom(n_words=W, n_routes=R, route_mode=mode, decide_thr=thr,
+                         cohort_sizes=sizes, n_steps=T, seed_key=9500 + case, ld=N + pad)
+    C = inp.n_cohorts
+    say("two-lane case %d: W=%d R=%d mode=%d thr=%d C=%d N=%d T=%d step0=%d"
+        % (case, W, R, mode, thr, C, N, T, step0))
+    want = orc.run_inputs(inp, n_steps=T, step0=step0)
+    rng = np.random.Generator(np.random.PCG64(93_000 + case))
+    cuts = sorted(set([0, C] + [int(x) for x in rng.integers(0, C + 1, size=2)]))
+    ranges = [(cuts[i], cuts[i + 1]) for i in range(len(cuts) - 1)]
+    rng.shuffle(ranges)
+    for label, mode_run, rr in (("resident", rc.RC_MODE_RESIDENT, [(0, C)]),
+                                ("resident ranges", rc.RC_MODE_RESIDENT, ranges),
+                                ("host round trip", rc.RC_MODE_HOST_ROUNDTRIP, [(0, C)])):
+        co = rc.Cohort.from_inputs(inp, max_steps=T)
+        try:
+            for cb, ce in rr:
+                co.run_chain(step0, T, mode_run, cb, ce)
+            got = co.download(T)
+        finally:
+            co.close()
+        assert_same(got, want, "two-lane case %d %s" % (case, label))
