@@ -827,9 +827,6 @@ __device__ __forceinline__ void wait_vmcnt() {
 // with the staging loads, later chunks' a chunk ahead).
 template <int WMAX, bool EXACT, int NWAVE, int RK, bool MULTI, bool SPLIT, bool FLOOR, bool PIPED>
 struct ChainF {
-    // Effect stores stay on the normal path: cohorts spanning wavefronts
-    // fill each line from several wavefronts.
-    static constexpr bool NTE = false;
     static constexpr uint32_t CNT_STRIDE = NWAVE + 4;
     // Words per lane.  SPLIT: an A lane holds words [0, WA) of its session
     // and emits the effects; its B lane holds words [WA, WMAX).  At
@@ -857,6 +854,18 @@ struct ChainF {
     static constexpr int TC = PIPE ? 4 : WMAX <= 32 ? 16 : 8;
     static constexpr uint32_t WG = (SPLIT ? 2 : 1) * NWAVE * 64;
     static constexpr int SB = WMAX <= 32 ? (SPLIT ? 5 : 10) : (SPLIT ? 3 : 6);
+    static constexpr uint32_t NLA = NWAVE * 64;  // lanes of the plan's sessions (the A lanes)
+    // Bins of sub-wavefront cohorts (each cohort inside one wavefront) pass
+    // their effects through an LDS stage: the lane of a session writes its
+    // effect at the stage position of the lane that holds the session
+    // numbered like the effect's slot, and reads back the effect whose slot
+    // is its own session index -- one wavefront, so LDS order is all the
+    // synchronization needed.  A wavefront's stores then cover its
+    // sessions' contiguous slots, whole cache lines, and go out
+    // nontemporal.  Cohorts spanning wavefronts store each effect directly
+    // at its slot through the L2, which merges the lines that several
+    // wavefronts fill (an LDS exchange across wavefronts at every step
+    // costs more than it saves).
 
     static __device__ __forceinline__ uint4 lds128(const uint32_t* lds, uint32_t byte_off) {
         return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(lds) + byte_off);
@@ -875,11 +884,16 @@ struct ChainF {
         const uint32_t R = a.ra.n_routes;
         const uint32_t T = a.n_steps;
         // The host reserves 16 steps of each: counts [16][NWAVE + 4], then
-        // (SPLIT) the control handed to the B lanes, [16][2][NWAVE * 64].
-        // PIPE uses the first 2 TC steps of both (two chunks in flight).
+        // (SPLIT) the control handed to the B lanes -- addends [16][NLA] and
+        // 16-bit control words [16][NLA] -- then the effect stage of
+        // sub-wavefront bins.  PIPE uses the first 2 TC steps of the count and control
+        // areas (two chunks in flight).
         static_assert(TC <= 16 && (!PIPE || 2 * TC <= 16), "LDS control and count areas hold 16 steps");
         uint32_t* lds_cnt = lds + a.img_words;
-        uint32_t* lds_x = lds_cnt + 16 * CNT_STRIDE;
+        uint32_t* lds_add = lds_cnt + 16 * CNT_STRIDE;
+        uint16_t* lds_ctl = reinterpret_cast<uint16_t*>(lds_add + (SPLIT ? 16 * NLA : 0));
+        uint32_t* stage_w = reinterpret_cast<uint32_t*>(lds_ctl + (SPLIT ? 16 * NLA : 0));
+        uint4* stage_p = reinterpret_cast<uint4*>(stage_w + NLA);
         const uint32_t* lds_tools = lds + a.tools_off;
 
         const uint32_t* lds_rows = lds + a.rows_off;
@@ -1105,8 +1119,8 @@ struct ChainF {
                 if constexpr (SPLIT) {
 #pragma unroll
                     for (int i = 0; i < TC; ++i) {
-                        lds_x[(2 * (par + i)) * (NWAVE * 64) + alane] = ctl[i];
-                        lds_x[(2 * (par + i) + 1) * (NWAVE * 64) + alane] = add[i];
+                        lds_ctl[(par + i) * NLA + alane] = (uint16_t)ctl[i];  // ctl < 2^16
+                        lds_add[(par + i) * NLA + alane] = add[i];
                     }
                 }
                 __builtin_amdgcn_s_setprio(0);
@@ -1121,6 +1135,7 @@ struct ChainF {
         // read the zero row (valid addresses, values unused).  The step count
         // is re-read so that no per-step condition stays live across the
         // phases.
+        const uint32_t my = alane;  // this lane's stage position
         auto replay = [&](uint32_t t0, auto qlo_c, auto qhi_c, auto eff_c, auto pref_c) {
             constexpr int QLO = decltype(qlo_c)::value;
             constexpr int QHI = decltype(qhi_c)::value;
@@ -1204,11 +1219,34 @@ struct ChainF {
                         // (a7) emit; slot - b < k always holds (the test keeps
                         // a compaction defect from becoming a write outside
                         // the cohort)
-                        if (L.active && slot - L.b < L.k) {
-                            st32<NTE>(p_sid, slot << 2, L.s);
-                            st32<NTE>(p_tool, slot << 2, tool);
-                            st128<NTE>(p_pay, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
-                            if (in_c == 0u) st32(p_cnt, L.c << 2, n1);
+                        const bool put = L.active && slot - L.b < L.k;
+                        if constexpr (MULTI) {
+                            if (put) {
+                                st32(p_sid, slot << 2, L.s);
+                                st32(p_tool, slot << 2, tool);
+                                st128(p_pay, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
+                                if (in_c == 0u) st32(p_cnt, L.c << 2, n1);
+                            }
+                        } else {
+                            // a cohort's sessions sit in consecutive lanes,
+                            // so session `slot` is held at stage position
+                            // my + (slot - s); sid < 2^28 leaves room for
+                            // the tool
+                            if (put) {
+                                const uint32_t pos = my + (slot - L.s);
+                                stage_w[pos] = L.s | (tool << 28);
+                                stage_p[pos] = make_uint4(S[0], S[1], S[2], S[3]);
+                            }
+                            asm volatile("" ::: "memory");
+                            if (L.active) {
+                                const uint32_t w = stage_w[my];
+                                const uint4 pv = stage_p[my];
+                                st32<true>(p_sid, soff, w & 0x0FFFFFFFu);
+                                st32<true>(p_tool, soff, w >> 28);
+                                st128<true>(p_pay, soff << 2, pv);
+                                if (in_c == 0u) st32(p_cnt, L.c << 2, n1);
+                            }
+                            asm volatile("" ::: "memory");  // this step's reads before the next step's writes
                         }
                         p_sid += ldw;
                         p_tool += ldw;
@@ -1290,8 +1328,8 @@ struct ChainF {
                     const uint32_t par = half_of(t0);
 #pragma unroll
                     for (int i = 0; i < TC; ++i) {
-                        ctl[i] = lds_x[(2 * (par + i)) * (NWAVE * 64) + alane];
-                        add[i] = lds_x[(2 * (par + i) + 1) * (NWAVE * 64) + alane];
+                        ctl[i] = lds_ctl[(par + i) * NLA + alane];
+                        add[i] = lds_add[(par + i) * NLA + alane];
                     }
                 };
                 read_ctl(0u);
@@ -1341,8 +1379,8 @@ struct ChainF {
                 auto read_ctl = [&]() {
 #pragma unroll
                     for (int i = 0; i < TC; ++i) {
-                        ctl[i] = lds_x[(2 * i) * (NWAVE * 64) + alane];
-                        add[i] = lds_x[(2 * i + 1) * (NWAVE * 64) + alane];
+                        ctl[i] = lds_ctl[i * NLA + alane];
+                        add[i] = lds_add[i * NLA + alane];
                     }
                 };
                 read_ctl();
@@ -2111,11 +2149,14 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     h->nwave = h->full ? 4u : 8u;
     // image, then the count exchange ([16][nwave + 4] words; the table chain
     // uses the first [2][nwave + 4]), then (full image, W >= 32: two lanes
-    // per session) the control handed to the second lanes, [16][2][nwave * 64]
+    // per session) the control handed to the second lanes, 16 steps of a
+    // 4-byte addend and a 2-byte control word per lane, then (full image)
+    // the effect stage of sub-wavefront bins, 4 + 16 bytes per lane
     const bool split = h->full && h->wmax >= 32u;
-    h->chain_threads = (split ? 2u : 1u) * h->nwave * 64u;
-    h->chain_lds_bytes = lds_image + 16u * (h->nwave + 4u) * 4u +
-                         (split ? 16u * 2u * h->nwave * 64u * 4u : 0u);
+    const uint32_t na = h->nwave * 64u;
+    h->chain_threads = (split ? 2u : 1u) * na;
+    h->chain_lds_bytes = lds_image + 16u * (h->nwave + 4u) * 4u + (split ? 16u * na * 6u : 0u) +
+                         (h->full ? na * 20u : 0u);
 
     h->offsets.assign(desc->cohort_offsets, desc->cohort_offsets + h->C + 1u);
     build_plan(h->offsets.data(), h->C, h->nwave, h->plan);
