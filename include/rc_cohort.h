@@ -151,13 +151,23 @@ int rc_cohort_step(rc_cohort *h, const rc_buffers *b, uint32_t step,
  * RC_MODE_RESIDENT enqueues one kernel launch and returns without waiting.
  * RC_MODE_HOST_ROUNDTRIP synchronizes the stream once per step (that
  * observation is the mechanism being measured) and returns after enqueuing
- * the last body kernel.  n_steps == 0 or an empty cohort range is a no-op.
- * Chains compose: (T1 steps from step0) then (T2 steps from step0 + T1)
- * equals T1 + T2 steps from step0.
+ * the last body kernel.  Its per-step scratch (a slot permutation and two
+ * counter words) belongs to the handle; a host-round-trip call first makes
+ * its stream wait for the previous host-round-trip call on the same handle
+ * (an event the handle records after that call's last body kernel), so
+ * calls on different streams never share the scratch.  n_steps == 0 or an
+ * empty cohort range is a no-op.  Chains compose: (T1 steps from step0)
+ * then (T2 steps from step0 + T1) equals T1 + T2 steps from step0.
+ * Buffer checks: the six buffers must lie inside HIP allocations of the
+ * handle's device, each inside one.  The check sees allocations as the HIP
+ * runtime made them, so a buffer carved out of a larger allocation (a block
+ * of a caching allocator, say) passes whenever it stays inside that
+ * allocation: sizing each buffer for its extent is the caller's part.  The
+ * handle remembers the last 16 buffer sets (pointers and extents) that
+ * passed and does not query the runtime again for them.
  * Errors: RC_E_INVALID for a NULL handle/buffer, ld < N, a bad range or
- * mode, overlapping buffers, or a buffer that is not device memory of the
- * handle's device large enough for its extent; RC_E_DEVICE when a launch or
- * copy fails.
+ * mode, overlapping buffers, or a buffer outside the allocations of the
+ * handle's device; RC_E_DEVICE when a launch or copy fails.
  */
 int rc_cohort_run_chain(rc_cohort *h, const rc_buffers *b, uint32_t step0,
                         uint32_t n_steps, int mode, uint32_t cohort_begin,

@@ -8,7 +8,8 @@ import subprocess
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "rc_cohort.hip")
-SRC_HOST = os.path.join(PKG, "csrc", "rc_pack.cpp")  # host-only part (cohort shares)
+SRC_HOST = [os.path.join(PKG, "csrc", "rc_host.cpp"),   # descriptor checks and launch plan
+            os.path.join(PKG, "csrc", "rc_pack.cpp")]   # cohort shares and online compactor
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librc_cohort.so")
 ARCH = "gfx950"
@@ -29,10 +30,10 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    """Compile ``csrc/rc_cohort.hip`` and ``csrc/rc_pack.cpp`` into
-    ``librc_cohort.so`` (always)."""
+    """Compile ``csrc/rc_cohort.hip``, ``csrc/rc_host.cpp`` and
+    ``csrc/rc_pack.cpp`` into ``librc_cohort.so`` (always)."""
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INCLUDE, "-o", tmp, SRC, SRC_HOST]
+    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INCLUDE, "-o", tmp, SRC] + SRC_HOST
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -70,10 +70,13 @@
 #include <vector>
 
 #include "rc_cohort.h"
+#include "rc_plan.h"
 
 
 
 namespace {
+
+using namespace rc_plan;
 
 // ---------------------------------------------------------------------------
 // Device helpers
@@ -178,28 +181,6 @@ __device__ __forceinline__ void st128(uint32_t* base, uint32_t byte_off, uint4 v
     if constexpr (NT) __builtin_nontemporal_store(x, p);
     else *p = x;
 }
-
-// Wavefront descriptor of the launch plan (16 x u32).
-enum : uint32_t {
-    WD_S0 = 0,        // session of lane 0
-    WD_NACT = 1,      // lanes [0, n_act) are active
-    WD_CFIRST = 2,    // cohort of lane 0
-    WD_NCOH = 3,      // cohorts present in this wavefront
-    WD_BFIRST = 4,    // first session of cohort c_first
-    WD_KFIRST = 5,    // size of cohort c_first
-    WD_FLAGS = 6,
-    WD_LIST = 8,      // sub-wavefront cohorts, in lane order: cohort q takes the
-                      // next k_q lanes, which hold its sessions in order
-    WD_MAXC = 8,      // at most this many cohorts per wavefront
-    WD_WORDS = 16
-};
-enum : uint32_t {
-    WF_MULTI = 1u,    // this wavefront is part of a cohort of > 64 sessions
-    WF_WGMULTI = 2u,  // some wavefront of the workgroup is (uniform per WG)
-    // bits 8..15: index of this wavefront inside its cohort
-    // bits 16..23: wavefronts of the cohort (at most 4)
-    // bits 24..31: first wavefront (inside the workgroup) of the cohort
-};
 
 struct RouteArgs {
     uint32_t mode;        // RC_ROUTE_MOD / RC_ROUTE_CDF
@@ -1446,13 +1427,13 @@ struct DecideArgs {
     const uint32_t* state;
     const uint32_t* outcome;
     uint32_t* n_taken;
-    uint32_t* perm;           // [N]
+    uint32_t* perm;           // slot j of the stepped range at perm[j - perm_lo]
     uint32_t* ctr;            // [2]
     const uint32_t* offsets;
     const uint32_t* wdesc;
     uint32_t thr, step, t_index, n_cohorts, n_sessions;
     uint32_t cohort_begin, cohort_end;
-    uint32_t bins_a_lo, bins_a_n, bins_b_lo, parity;
+    uint32_t bins_a_lo, bins_a_n, bins_b_lo, parity, perm_lo;
 };
 
 template <int NWAVE>
@@ -1484,7 +1465,7 @@ __global__ __launch_bounds__(NWAVE * 64) void rc_decide_kernel(DecideArgs a) {
     uint32_t n1;
     const uint32_t slot = slot_of(L, dk, bal, c4, n1);
     if (L.active && L.s == L.b) a.n_taken[(size_t)a.t_index * a.n_cohorts + L.c] = n1;
-    if (L.active && slot - L.b < L.k) a.perm[slot] = L.s | (dk ? 0x80000000u : 0u);
+    if (L.active && slot - L.b < L.k) a.perm[slot - a.perm_lo] = L.s | (dk ? 0x80000000u : 0u);
     if (lane == 0u && bal) atomicAdd(&wg_taken, (uint32_t)__popcll(bal));
     __syncthreads();
     if (tid == 0u && wg_taken) atomicAdd(&a.ctr[a.parity], wg_taken);
@@ -1499,7 +1480,7 @@ struct BodyArgs {
     uint32_t* eff_sid;
     uint32_t* eff_tool;
     uint32_t* eff_payload;
-    const uint32_t* perm;
+    const uint32_t* perm;  // slot j at perm[j - lo]
     const uint32_t* raw;   // [R][16]
     const uint32_t* cdf;
     RouteArgs ra;
@@ -1516,7 +1497,7 @@ __global__ __launch_bounds__(256) void rc_body_kernel(BodyArgs a) {
     }
     const uint32_t slot = a.lo + blockIdx.x * 256u + tid;
     if (slot >= a.hi) return;
-    const uint32_t e = a.perm[slot];
+    const uint32_t e = a.perm[slot - a.lo];
     if ((e >> 31) != (TAKEN ? 1u : 0u)) return;
     const uint32_t s = e & 0x7FFFFFFFu;
     if (s >= a.n_sessions) return;  // never taken by a valid permutation
@@ -1545,6 +1526,13 @@ __global__ __launch_bounds__(256) void rc_body_kernel(BodyArgs a) {
     st32(a.eff_tool + slice, slot << 2, (a.raw[r * 16u + (TAKEN ? 1u : 0u)]) & 7u);
     st128(a.eff_payload + slice * 4u, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
     st32(a.outcome, soff, dev_fmix32(S[0]));
+}
+
+// Clears n words (a kernel rather than a memset, so that callers that
+// capture the work into a graph record no memset node).
+__global__ __launch_bounds__(64) void rc_clear_kernel(uint32_t* p, uint32_t n) {
+    const uint32_t i = blockIdx.x * 64u + threadIdx.x;
+    if (i < n) p[i] = 0u;
 }
 
 // ---------------------------------------------------------------------------
@@ -1596,8 +1584,8 @@ ChainFn pick_chain(uint32_t wmax, bool exact, bool full, bool piped, int rk, boo
 // at most one workgroup per CU.  Measured on MI355X (256-session cohorts,
 // W = 32): 6-10% faster than the two-role split from 1 to 256 workgroups at
 // T = 32, slower beyond that and at every size for T <= 16.
-bool use_piped(uint32_t wmax, bool full, uint32_t T, uint32_t grid) {
-    return has_piped(wmax, full) && T > 16u && grid <= 256u;
+bool use_piped(uint32_t wmax, bool full, uint32_t T, uint32_t grid, uint32_t n_cu) {
+    return has_piped(wmax, full) && T > 16u && grid <= n_cu;
 }
 
 template <int WMAX, bool EXACT>
@@ -1645,19 +1633,17 @@ uint32_t ceil_log2(uint32_t x) {
     return g;
 }
 
-// The launch plan: per-wavefront descriptors plus the lookups that turn a
-// cohort range into bin ranges.  Built on the host, without a device.
-struct Plan {
-    uint32_t nwave = 4;
-    uint32_t n_bins = 0, n_bins_a = 0, idle_lanes = 0;
-    std::vector<uint32_t> wdesc;             // [bins][nwave][WD_WORDS]
-    std::vector<uint32_t> bin_of_cohort;     // [C]
-    std::vector<uint32_t> first_a, first_b;  // [C+1]: first cohort >= c of the class (C if none)
-    std::vector<int32_t> last_a, last_b;     // [C]: last cohort <= c of the class (-1 if none)
+// Validated buffer sets remembered per handle (see validate_buffers).
+constexpr int EXTENT_CACHE = 16;
+struct BufferKey {
+    const void* p[7];
+    uint64_t bytes[7];
+    bool operator==(const BufferKey& o) const {
+        for (int i = 0; i < 7; ++i)
+            if (p[i] != o.p[i] || bytes[i] != o.bytes[i]) return false;
+        return true;
+    }
 };
-
-constexpr size_t FULL_IMAGE_LIMIT = 72u * 1024u;  // bytes of the full mask image
-constexpr size_t LDS_TWO_PER_CU = 80u * 1024u;    // two workgroups per CU fit below this
 
 }  // namespace
 
@@ -1687,6 +1673,14 @@ struct rc_cohort {
     uint32_t parity = 0;
     bool ctr_dirty = false;
     uint32_t last_launches = 0, last_d2h = 0;
+    // Recorded after the last body kernel of a host-round-trip call; the next
+    // such call's stream waits for it before touching d_perm / d_ctr.
+    hipEvent_t hrt_done = nullptr;
+    bool hrt_pending = false;
+    uint32_t n_cu = 256;             // compute units of the device
+    size_t lds_per_cu = 160u * 1024u;
+    BufferKey seen[EXTENT_CACHE];    // buffer sets that passed the device checks
+    int n_seen = 0, next_seen = 0;
 };
 
 namespace {
@@ -1704,187 +1698,11 @@ void free_handle(rc_cohort* h) {
         (void)hipFree(h->d_perm);
         (void)hipFree(h->d_ctr);
         if (h->h_word) (void)hipHostFree(h->h_word);
+        if (h->hrt_done) (void)hipEventDestroy(h->hrt_done);
     }
     delete h;
 }
 
-int validate_desc(const rc_cohort_desc* d) {
-    if (!d) return RC_E_INVALID;
-    if (d->n_sessions < 1u || d->n_sessions > RC_MAX_SESSIONS) return RC_E_INVALID;
-    if (d->n_words < RC_MIN_WORDS || d->n_words > RC_MAX_WORDS) return RC_E_INVALID;
-    if (d->n_routes < 1u || d->n_routes > RC_MAX_ROUTES) return RC_E_INVALID;
-    if (d->n_cohorts < 1u || d->n_cohorts > d->n_sessions) return RC_E_INVALID;
-    if (!d->cohort_offsets || !d->table) return RC_E_INVALID;
-    if (d->route_mode != RC_ROUTE_MOD && d->route_mode != RC_ROUTE_CDF) return RC_E_INVALID;
-    if (d->decide_thr > 65536u) return RC_E_INVALID;
-    const uint32_t* off = d->cohort_offsets;
-    if (off[0] != 0u || off[d->n_cohorts] != d->n_sessions) return RC_E_INVALID;
-    for (uint32_t c = 0; c < d->n_cohorts; ++c) {
-        if (off[c + 1] <= off[c]) return RC_E_INVALID;
-        if (off[c + 1] - off[c] > RC_MAX_COHORT) return RC_E_INVALID;
-    }
-    if (d->route_mode == RC_ROUTE_CDF && d->n_routes > 1u) {
-        if (!d->route_cdf) return RC_E_INVALID;
-        for (uint32_t k = 1; k + 1u < d->n_routes; ++k)
-            if (d->route_cdf[k] < d->route_cdf[k - 1]) return RC_E_INVALID;
-    }
-    return RC_OK;
-}
-
-// Pack cohorts into bins of nw wavefronts (see the file comment): first every
-// cohort of at most 64 sessions, in order, each into the first wavefront of
-// the open bin with room for it (at most WD_MAXC cohorts per wavefront), then
-// the larger ones.  A cohort never goes to an earlier bin than the one
-// before it, so the bins of a cohort range are contiguous.
-void build_plan(const uint32_t* off, uint32_t C, uint32_t nw_per_bin, Plan& P) {
-    const uint32_t NW = nw_per_bin;
-    P.nwave = NW;
-    P.wdesc.clear();
-    P.bin_of_cohort.assign(C, 0);
-    int64_t bin = -1;        // open bin (-1: none)
-    uint32_t wave = 0, lane = 0;
-    // sub-wavefront class: free lanes and cohorts of the open bin's wavefronts
-    std::vector<uint32_t> room(NW, 0u), ncoh(NW, 0u);
-    uint32_t started = 0;    // wavefronts started in the open bin
-    // multi-wavefront class: the bin before the open one, still open
-    int64_t prev_bin = -1;
-    uint32_t prev_used = 0;
-    auto open_bin = [&]() {
-        ++bin;
-        wave = 0;
-        lane = 0;
-        started = 0;
-        P.wdesc.resize((size_t)(bin + 1) * NW * WD_WORDS, 0u);
-    };
-    auto place = [&](uint32_t c) {
-        const uint32_t b = off[c], k = off[c + 1] - off[c];
-        if (k > 64u) {
-            // The previous bin stays open beside the current one: a cohort
-            // goes into the first of the two with nw free wavefronts left,
-            // else into a new bin (which retires the previous one).  So a
-            // cohort lands at most one bin before the one of any cohort
-            // placed earlier; bins_of_range widens its range by one.
-            const uint32_t nw = (k + 63u) / 64u;
-            int64_t tb;
-            uint32_t tw;
-            if (prev_bin >= 0 && prev_used + nw <= NW) {
-                tb = prev_bin;
-                tw = prev_used;
-                prev_used += nw;
-            } else {
-                if (bin < 0 || wave + nw > NW) {
-                    prev_bin = bin;  // -1 before the class's first bin
-                    prev_used = wave;
-                    open_bin();
-                }
-                tb = bin;
-                tw = wave;
-                wave += nw;
-            }
-            for (uint32_t i = 0; i < nw; ++i) {
-                uint32_t* d = &P.wdesc[((size_t)tb * NW + tw + i) * WD_WORDS];
-                d[WD_S0] = b + 64u * i;
-                d[WD_NACT] = (k - 64u * i) < 64u ? (k - 64u * i) : 64u;
-                d[WD_CFIRST] = c;
-                d[WD_NCOH] = 1;
-                d[WD_BFIRST] = b;
-                d[WD_KFIRST] = k;
-                d[WD_FLAGS] = WF_MULTI | (i << 8) | (nw << 16) | (tw << 24);
-            }
-            P.bin_of_cohort[c] = (uint32_t)tb;
-        } else {
-            // first fit among the wavefronts of the open bin (so that the
-            // bins of a cohort range stay together), then a new wavefront
-            uint32_t w = NW;
-            if (bin >= 0)
-                for (uint32_t q = 0; q < started; ++q)
-                    if (room[q] >= k && ncoh[q] < WD_MAXC) { w = q; break; }
-            if (w == NW) {
-                if (bin < 0 || started == NW) open_bin();
-                w = started++;
-                room[w] = 64u;
-                ncoh[w] = 0u;
-                uint32_t* d = &P.wdesc[((size_t)bin * NW + w) * WD_WORDS];
-                d[WD_S0] = b;
-                d[WD_NACT] = 0;
-                d[WD_CFIRST] = c;
-                d[WD_NCOH] = 0;
-                d[WD_BFIRST] = b;
-                d[WD_KFIRST] = k;
-                d[WD_FLAGS] = 0;
-            }
-            uint32_t* d = &P.wdesc[((size_t)bin * NW + w) * WD_WORDS];
-            d[WD_LIST + ncoh[w]] = c;
-            d[WD_NCOH] = ++ncoh[w];
-            d[WD_NACT] += k;
-            room[w] -= k;
-            P.bin_of_cohort[c] = (uint32_t)bin;
-        }
-    };
-    for (uint32_t c = 0; c < C; ++c)
-        if (off[c + 1] - off[c] <= 64u) place(c);
-    P.n_bins_a = (uint32_t)(bin + 1);
-    wave = NW;  // the multi-wavefront class starts in a fresh bin
-    lane = 0;
-    prev_bin = -1;
-    for (uint32_t c = 0; c < C; ++c)
-        if (off[c + 1] - off[c] > 64u) place(c);
-    P.n_bins = (uint32_t)(bin + 1);
-
-    // class lookups for cohort ranges
-    P.first_a.assign(C + 1u, C);
-    P.first_b.assign(C + 1u, C);
-    for (int64_t c = (int64_t)C - 1; c >= 0; --c) {
-        const bool small = off[c + 1] - off[c] <= 64u;
-        P.first_a[c] = small ? (uint32_t)c : P.first_a[c + 1];
-        P.first_b[c] = small ? P.first_b[c + 1] : (uint32_t)c;
-    }
-    P.last_a.assign(C, -1);
-    P.last_b.assign(C, -1);
-    for (uint32_t c = 0; c < C; ++c) {
-        const bool small = off[c + 1] - off[c] <= 64u;
-        P.last_a[c] = small ? (int32_t)c : (c ? P.last_a[c - 1] : -1);
-        P.last_b[c] = small ? (c ? P.last_b[c - 1] : -1) : (int32_t)c;
-    }
-
-    // mark workgroups that contain a multi-wavefront cohort; count idle lanes
-    uint32_t idle = 0;
-    for (uint32_t bb = 0; bb < P.n_bins; ++bb) {
-        bool any = false;
-        for (uint32_t w = 0; w < NW; ++w) any |= (P.wdesc[((size_t)bb * NW + w) * WD_WORDS + WD_FLAGS] & WF_MULTI) != 0u;
-        for (uint32_t w = 0; w < NW; ++w) {
-            uint32_t* d = &P.wdesc[((size_t)bb * NW + w) * WD_WORDS];
-            if (any) d[WD_FLAGS] |= WF_WGMULTI;
-            idle += 64u - d[WD_NACT];
-        }
-    }
-    P.idle_lanes = idle;
-}
-
-// Bins covering the cohorts [cb, ce) (cb < ce): a range of sub-wavefront
-// bins and a range of multi-wavefront bins.
-void bins_of_range(const Plan& P, uint32_t cb, uint32_t ce, uint32_t& a_lo, uint32_t& a_n,
-                   uint32_t& b_lo, uint32_t& b_n) {
-    a_lo = a_n = b_lo = b_n = 0;
-    const uint32_t fa = P.first_a[cb];
-    if (fa < ce) {
-        const uint32_t la = (uint32_t)P.last_a[ce - 1];
-        a_lo = P.bin_of_cohort[fa];
-        a_n = P.bin_of_cohort[la] - a_lo + 1u;
-    }
-    const uint32_t fb = P.first_b[cb];
-    if (fb < ce) {
-        // a multi-wavefront cohort lies at most one bin before the bin of
-        // any cohort placed earlier (build_plan), so the range's cohorts lie
-        // within one bin of [bin(first), bin(last)]; cohorts of the extra
-        // bins outside [cb, ce) are masked off in the kernels
-        const uint32_t lb = (uint32_t)P.last_b[ce - 1];
-        const uint32_t lo = P.bin_of_cohort[fb] > P.n_bins_a ? P.bin_of_cohort[fb] - 1u : P.n_bins_a;
-        const uint32_t hi = P.bin_of_cohort[lb] + 1u < P.n_bins ? P.bin_of_cohort[lb] + 1u : P.n_bins - 1u;
-        b_lo = lo;
-        b_n = hi - lo + 1u;
-    }
-}
 
 template <typename T>
 int dev_upload(T** dst, const void* src, size_t bytes) {
@@ -1908,8 +1726,11 @@ bool device_extent_ok(const void* p, size_t bytes, int dev) {
 }
 
 // The caller's buffers (and, for the no-decision floor, its decision
-// bitmap): present, inside one device allocation each, pairwise disjoint.
-int validate_buffers(const rc_cohort* h, const rc_buffers* b, uint32_t T, bool floor = false,
+// bitmap): present, pairwise disjoint, and each inside one device allocation
+// of the handle's device.  The allocation check queries the HIP runtime; a
+// buffer set (pointers and extents) that passed it is remembered, and the
+// last EXTENT_CACHE such sets are not queried again.
+int validate_buffers(rc_cohort* h, const rc_buffers* b, uint32_t T, bool floor = false,
                      const uint32_t* dbits = nullptr) {
     if (!b) return RC_E_INVALID;
     if (b->ld < h->N || b->ld > RC_MAX_SESSIONS) return RC_E_INVALID;
@@ -1934,8 +1755,18 @@ int validate_buffers(const rc_cohort* h, const rc_buffers* b, uint32_t T, bool f
             const uintptr_t b0 = (uintptr_t)ext[j].p, b1 = b0 + ext[j].bytes;
             if (a0 < b1 && b0 < a1) return RC_E_INVALID;
         }
+    BufferKey key;
+    for (int i = 0; i < 7; ++i) {
+        key.p[i] = i < n ? ext[i].p : nullptr;
+        key.bytes[i] = i < n ? ext[i].bytes : 0u;
+    }
+    for (int i = 0; i < h->n_seen; ++i)
+        if (h->seen[i] == key) return RC_OK;
     for (int i = 0; i < n; ++i)
         if (ext[i].bytes && !device_extent_ok(ext[i].p, ext[i].bytes, h->device)) return RC_E_INVALID;
+    h->seen[h->next_seen] = key;
+    h->next_seen = (h->next_seen + 1) % EXTENT_CACHE;
+    if (h->n_seen < EXTENT_CACHE) ++h->n_seen;
     return RC_OK;
 }
 
@@ -1974,7 +1805,7 @@ int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
     a.dbits = dbits;
     a.dwords = (b->ld + 31u) / 32u;
     const uint32_t grid = a.bins_a_n + a.bins_b_n;  // one workgroup per bin
-    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, use_piped(h->wmax, h->full, T, grid),
+    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, use_piped(h->wmax, h->full, T, grid, h->n_cu),
                             h->route_kind, dbits != nullptr);
     hipLaunchKernelGGL(fn, dim3(grid), dim3(h->chain_threads), h->chain_lds_bytes, stream, a);
     if (launch_ok() != RC_OK) return RC_E_DEVICE;
@@ -1983,14 +1814,30 @@ int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
     return RC_OK;
 }
 
+// Where a host-round-trip call keeps its per-step scratch: the
+// slot-to-session permutation of the stepped range (slot j at
+// perm[j - lo]) and the two counter words of the 4-byte observation, plus
+// the event that orders the calls sharing them.
+struct HrtScratch {
+    uint32_t* perm;
+    uint32_t* ctr;
+    uint32_t* parity;   // which counter word the next step adds to
+    hipEvent_t done;    // recorded after a call's last body kernel
+    bool* pending;      // `done` has been recorded
+    bool clear_first;   // clear both counter words with a kernel first
+};
+
 int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
-                       uint32_t cb, uint32_t ce, hipStream_t stream) {
+                       uint32_t cb, uint32_t ce, hipStream_t stream, const HrtScratch& sc) {
     uint32_t launches = 0, copies = 0;
-    if (h->ctr_dirty) {
-        // a previous call stopped inside a step: restart from cleared counters
-        if (hipMemsetAsync(h->d_ctr, 0, 2 * sizeof(uint32_t), stream) != hipSuccess) return RC_E_DEVICE;
-        h->parity = 0;
-        h->ctr_dirty = false;
+    // the previous call that used this scratch may still be running on
+    // another stream: wait for its last body kernel
+    if (*sc.pending && hipStreamWaitEvent(stream, sc.done, 0) != hipSuccess) return RC_E_DEVICE;
+    if (sc.clear_first) {
+        hipLaunchKernelGGL(rc_clear_kernel, dim3(1), dim3(64), 0, stream, sc.ctr, 2u);
+        if (launch_ok() != RC_OK) return RC_E_DEVICE;
+        ++launches;
+        *sc.parity = 0;
     }
     uint32_t a_lo, a_n, b_lo, b_n;
     bins_of_range(h->plan, cb, ce, a_lo, a_n, b_lo, b_n);
@@ -2002,13 +1849,13 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
     BodyFn taken_fn = pick_body(h->wmax, h->exact, true);
     BodyFn not_fn = pick_body(h->wmax, h->exact, false);
     for (uint32_t t = 0; t < T; ++t) {
-        h->ctr_dirty = true;  // cleared again when the step completes
+        if (!sc.clear_first) h->ctr_dirty = true;  // the handle's counters; cleared again when the step completes
         DecideArgs d;
         d.state = b->state;
         d.outcome = b->outcome;
         d.n_taken = b->n_taken;
-        d.perm = h->d_perm;
-        d.ctr = h->d_ctr;
+        d.perm = sc.perm;
+        d.ctr = sc.ctr;
         d.offsets = h->d_offsets;
         d.wdesc = h->d_wdesc;
         d.thr = h->thr;
@@ -2021,12 +1868,13 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
         d.bins_a_lo = a_lo;
         d.bins_a_n = a_n;
         d.bins_b_lo = b_lo;
-        d.parity = h->parity;
+        d.parity = *sc.parity;
+        d.perm_lo = lo;
         hipLaunchKernelGGL(dfn, dim3(grid), dim3(h->nwave * 64), 0, stream, d);
         if (launch_ok() != RC_OK) return RC_E_DEVICE;
         ++launches;
         // the observation: 4 bytes to pinned host memory, then wait
-        if (hipMemcpyAsync(h->h_word, h->d_ctr + h->parity, sizeof(uint32_t),
+        if (hipMemcpyAsync(h->h_word, sc.ctr + *sc.parity, sizeof(uint32_t),
                            hipMemcpyDeviceToHost, stream) != hipSuccess) return RC_E_DEVICE;
         ++copies;
         if (hipStreamSynchronize(stream) != hipSuccess) return RC_E_DEVICE;
@@ -2039,7 +1887,7 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
         ba.eff_sid = b->eff_sid;
         ba.eff_tool = b->eff_tool;
         ba.eff_payload = b->eff_payload;
-        ba.perm = h->d_perm;
+        ba.perm = sc.perm;
         ba.raw = h->d_raw;
         ba.cdf = h->d_cdf;
         ba.ra = h->ra;
@@ -2059,27 +1907,33 @@ int run_host_roundtrip(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32
             if (launch_ok() != RC_OK) return RC_E_DEVICE;
             ++launches;
         }
-        h->parity ^= 1u;
-        h->ctr_dirty = false;
+        *sc.parity ^= 1u;
+        if (!sc.clear_first) h->ctr_dirty = false;
     }
+    if (hipEventRecord(sc.done, stream) != hipSuccess) return RC_E_DEVICE;
+    *sc.pending = true;
     h->last_launches = launches;
     h->last_d2h = copies;
     return RC_OK;
 }
 
+// The handle's own scratch (d_perm, d_ctr), after restoring cleared counters
+// if a previous call stopped inside a step.
+int run_host_roundtrip_handle(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
+                              uint32_t cb, uint32_t ce, hipStream_t stream) {
+    if (h->ctr_dirty) {
+        if (h->hrt_pending && hipStreamWaitEvent(stream, h->hrt_done, 0) != hipSuccess) return RC_E_DEVICE;
+        if (hipMemsetAsync(h->d_ctr, 0, 2 * sizeof(uint32_t), stream) != hipSuccess) return RC_E_DEVICE;
+        h->parity = 0;
+        h->ctr_dirty = false;
+    }
+    HrtScratch sc{h->d_perm + h->offsets[cb], h->d_ctr, &h->parity, h->hrt_done, &h->hrt_pending, false};
+    return run_host_roundtrip(h, b, step0, T, cb, ce, stream, sc);
+}
+
 }  // namespace
 
 extern "C" {
-
-const char* rc_status_string(int status) {
-    switch (status) {
-        case RC_OK: return "RC_OK";
-        case RC_E_INVALID: return "RC_E_INVALID";
-        case RC_E_NOMEM: return "RC_E_NOMEM";
-        case RC_E_DEVICE: return "RC_E_DEVICE";
-        default: return "RC_E_UNKNOWN";
-    }
-}
 
 int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out) {
     if (!out) return RC_E_INVALID;
@@ -2092,12 +1946,19 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, hip_device) != hipSuccess) return RC_E_DEVICE;
     if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return RC_E_DEVICE;
+    if (prop.multiProcessorCount < 1 || prop.maxSharedMemoryPerMultiProcessor < 64u * 1024u) return RC_E_DEVICE;
 
     rc_cohort* h = new (std::nothrow) rc_cohort();
     if (!h) return RC_E_NOMEM;
     DeviceGuard guard(hip_device);
     if (!guard.ok) { delete h; return RC_E_DEVICE; }
     h->device = hip_device;
+    h->n_cu = (uint32_t)prop.multiProcessorCount;
+    h->lds_per_cu = prop.maxSharedMemoryPerMultiProcessor;
+    // the full mask image up to 45% of a CU's LDS (72 KB of 160 KB); two
+    // workgroups per CU below half of it
+    const size_t full_image_limit = h->lds_per_cu * 9u / 20u;
+    const size_t lds_two_per_cu = h->lds_per_cu / 2u;
     h->N = desc->n_sessions;
     h->W = desc->n_words;
     h->R = desc->n_routes;
@@ -2119,7 +1980,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
 
     // table image layout (see the file comment)
     const size_t full_bytes = (size_t)(R + 1u) * (h->wmax + 4u) * 4u;
-    h->full = h->wmax <= 16u || full_bytes <= FULL_IMAGE_LIMIT;
+    h->full = h->wmax <= 16u || full_bytes <= full_image_limit;
     // Full image: [word-0 masks | CDF thresholds | guide] (the chain
     // section, everything the word-0 chain reads), then the mask rows, then
     // the tool pairs.  Table image: the raw rows, then thresholds and guide.
@@ -2135,7 +1996,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
         const uint32_t gmin = ceil_log2(R) < 1u ? 1u : ceil_log2(R);
         guide_bits = gmin + 2u < 12u ? gmin + 2u : (gmin > 12u ? gmin : 12u);
         while (guide_bits > gmin &&
-               ((size_t)h->guide_off + pad4((1u << guide_bits) + 1u) + after_guide) * 4u + 256u > LDS_TWO_PER_CU)
+               ((size_t)h->guide_off + pad4((1u << guide_bits) + 1u) + after_guide) * 4u + 256u > lds_two_per_cu)
             --guide_bits;
         guide_n = (1u << guide_bits) + 1u;
         h->ra.guide_shift = 32u - guide_bits;
@@ -2173,6 +2034,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     if (rc == RC_OK && hipMalloc((void**)&h->d_ctr, 2 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_NOMEM;
     if (rc == RC_OK && hipMemset(h->d_ctr, 0, 2 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_DEVICE;
     if (rc == RC_OK && hipHostMalloc((void**)&h->h_word, sizeof(uint32_t), hipHostMallocDefault) != hipSuccess) rc = RC_E_NOMEM;
+    if (rc == RC_OK && hipEventCreateWithFlags(&h->hrt_done, hipEventDisableTiming) != hipSuccess) rc = RC_E_DEVICE;
     if (rc == RC_OK) {
         ImageArgs ia;
         ia.raw = h->d_raw;
@@ -2230,7 +2092,7 @@ int rc_cohort_run_chain(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint3
     if (n_steps == 0u || cohort_begin == cohort_end) return RC_OK;
     hipStream_t stream = (hipStream_t)hip_stream;
     if (mode == RC_MODE_RESIDENT) return run_resident(h, b, step0, n_steps, cohort_begin, cohort_end, stream);
-    return run_host_roundtrip(h, b, step0, n_steps, cohort_begin, cohort_end, stream);
+    return run_host_roundtrip_handle(h, b, step0, n_steps, cohort_begin, cohort_end, stream);
 }
 
 int rc_cohort_run_floor(rc_cohort* h, const rc_buffers* b, const uint32_t* decisions, uint32_t n_steps,
@@ -2270,44 +2132,6 @@ int rc_cohort_plan_info(const rc_cohort* h, uint32_t* n_workgroups, uint32_t* la
     if (n_workgroups) *n_workgroups = h->plan.n_bins;
     if (lanes_per_workgroup) *lanes_per_workgroup = h->nwave * 64u;
     if (idle_lanes) *idle_lanes = h->plan.idle_lanes;
-    return RC_OK;
-}
-
-int rc_plan_lanes(const rc_cohort_desc* desc, uint32_t lanes_per_workgroup, uint32_t* lane_session,
-                  uint32_t* lane_cohort_out, uint32_t capacity, uint32_t* n_lanes) {
-    if (!n_lanes) return RC_E_INVALID;
-    const int v = validate_desc(desc);
-    if (v != RC_OK) return v;
-    if (lanes_per_workgroup != 256u && lanes_per_workgroup != 512u) return RC_E_INVALID;
-    Plan P;
-    build_plan(desc->cohort_offsets, desc->n_cohorts, lanes_per_workgroup / 64u, P);
-    const uint32_t total = P.n_bins * lanes_per_workgroup;
-    *n_lanes = total;
-    if (!lane_session || !lane_cohort_out) return RC_OK;
-    if (capacity < total) return RC_E_INVALID;
-    const uint32_t* off = desc->cohort_offsets;
-    for (uint32_t wv = 0; wv < P.n_bins * P.nwave; ++wv) {
-        const uint32_t* d = &P.wdesc[(size_t)wv * WD_WORDS];
-        for (uint32_t lane = 0; lane < 64u; ++lane) {
-            // the per-lane derivation of lane_cohort() in the kernels
-            uint32_t s = d[WD_S0] + lane;
-            uint32_t c = d[WD_CFIRST];
-            if (d[WD_NCOH] > 1u) {
-                uint32_t at = 0u;
-                for (uint32_t q = 0; q < d[WD_NCOH]; ++q) {
-                    const uint32_t cq = d[WD_LIST + q];
-                    if (lane >= at) {
-                        c = cq;
-                        s = off[cq] + (lane - at);
-                    }
-                    at += off[cq + 1u] - off[cq];
-                }
-            }
-            const bool act = lane < d[WD_NACT];
-            lane_session[wv * 64u + lane] = act ? s : 0xFFFFFFFFu;
-            lane_cohort_out[wv * 64u + lane] = act ? c : 0xFFFFFFFFu;
-        }
-    }
     return RC_OK;
 }
 

@@ -18,7 +18,9 @@ from typing import Dict, Optional
 import numpy as np
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "librc_cohort.so")
+# RC_COHORT_LIB names another build of the same sources, e.g. the host-only
+# sanitizer build of the CPU tests (which holds no GPU entry point).
+LIB_PATH = os.environ.get("RC_COHORT_LIB") or os.path.join(PKG, "librc_cohort.so")
 
 RC_OK, RC_E_INVALID, RC_E_NOMEM, RC_E_DEVICE = 0, 1, 2, 3
 RC_ROUTE_MOD, RC_ROUTE_CDF = 0, 1
@@ -34,6 +36,9 @@ EXPORTED = [
     "rc_cohort_destroy", "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info",
     "rc_plan_lanes", "rc_pack_shares", "rc_online_compact", "rc_cohorts_from_batches",
 ]
+# entry points that need no device (the host-only build holds only these)
+HOST_ONLY = ["rc_status_string", "rc_plan_lanes", "rc_pack_shares", "rc_online_compact",
+             "rc_cohorts_from_batches"]
 
 _P32 = ctypes.POINTER(ctypes.c_uint32)
 
@@ -104,6 +109,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             "librc_cohort.so is not built (run paper_2608_12123_amd/build.py or "
             "__graft_entry__.build()); there is no CPU fallback")
     lib = ctypes.CDLL(path)
+    missing = [n for n in EXPORTED if not hasattr(lib, n)]
+    if missing and (path == os.path.join(PKG, "librc_cohort.so") or set(missing) & set(HOST_ONLY)):
+        raise RuntimeError("%s lacks %s" % (path, ", ".join(missing)))
+    if missing:
+        # a host-only build: declare only what it holds
+        _declare_host(lib)
+        _lib = lib
+        return lib
     lib.rc_cohort_create.argtypes = [ctypes.POINTER(RcCohortDesc), ctypes.c_int,
                                      ctypes.POINTER(ctypes.c_void_p)]
     lib.rc_cohort_create.restype = ctypes.c_int
@@ -120,12 +133,18 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rc_cohort_run_floor.restype = ctypes.c_int
     lib.rc_cohort_destroy.argtypes = [ctypes.c_void_p]
     lib.rc_cohort_destroy.restype = ctypes.c_int
-    lib.rc_status_string.argtypes = [ctypes.c_int]
-    lib.rc_status_string.restype = ctypes.c_char_p
     lib.rc_cohort_last_counts.argtypes = [ctypes.c_void_p, _P32, _P32]
     lib.rc_cohort_last_counts.restype = ctypes.c_int
     lib.rc_cohort_plan_info.argtypes = [ctypes.c_void_p, _P32, _P32, _P32]
     lib.rc_cohort_plan_info.restype = ctypes.c_int
+    _declare_host(lib)
+    _lib = lib
+    return lib
+
+
+def _declare_host(lib: ctypes.CDLL):
+    lib.rc_status_string.argtypes = [ctypes.c_int]
+    lib.rc_status_string.restype = ctypes.c_char_p
     lib.rc_plan_lanes.argtypes = [ctypes.POINTER(RcCohortDesc), ctypes.c_uint32, _P32, _P32,
                                   ctypes.c_uint32, _P32]
     lib.rc_plan_lanes.restype = ctypes.c_int
@@ -141,8 +160,6 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rc_cohorts_from_batches.argtypes = [_P32, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
                                             _P32, _P32, ctypes.POINTER(ctypes.c_uint64)]
     lib.rc_cohorts_from_batches.restype = ctypes.c_int
-    _lib = lib
-    return lib
 
 
 def _u32(a) -> np.ndarray:
@@ -347,8 +364,24 @@ def _to_host_u32(t) -> np.ndarray:
     return t.cpu().numpy().view(np.uint32)
 
 
-def buffers_of(tensors: Dict[str, "object"], ld: int) -> RcBuffers:
-    """An ``RcBuffers`` pointing at torch tensors (keys as in the C struct)."""
+def buffers_of(tensors: Dict[str, "object"], ld: int, n_words: Optional[int] = None,
+               n_steps: Optional[int] = None, n_cohorts: Optional[int] = None) -> RcBuffers:
+    """An ``RcBuffers`` pointing at torch tensors (keys as in the C struct).
+    Every tensor must be contiguous with 4-byte elements; given the shape
+    (W, T, C), each must also hold at least its extent for chains of up to
+    T steps (the library checks only that a buffer lies inside one device
+    allocation)."""
+    need = {"state": None if n_words is None else n_words * ld, "outcome": ld,
+            "eff_sid": None if n_steps is None else n_steps * ld,
+            "eff_tool": None if n_steps is None else n_steps * ld,
+            "eff_payload": None if n_steps is None else 4 * n_steps * ld,
+            "n_taken": None if n_steps is None or n_cohorts is None else n_steps * n_cohorts}
+    for k, n in need.items():
+        t = tensors[k]
+        if not t.is_contiguous() or t.element_size() != 4:
+            raise ValueError("buffer %s must be a contiguous tensor of 4-byte elements" % k)
+        if n is not None and t.numel() < n:
+            raise ValueError("buffer %s holds %d elements, needs %d" % (k, t.numel(), n))
     return RcBuffers(tensors["state"].data_ptr(), tensors["outcome"].data_ptr(),
                      tensors["eff_sid"].data_ptr(), tensors["eff_tool"].data_ptr(),
                      tensors["eff_payload"].data_ptr(), tensors["n_taken"].data_ptr(), ld)
@@ -378,7 +411,7 @@ class Cohort:
         mk = lambda *shape: torch.full(shape, fill32, dtype=torch.int32, device=self.device)
         self.t = {"state": mk(n_words, ld), "outcome": mk(ld), "eff_sid": mk(T, ld),
                   "eff_tool": mk(T, ld), "eff_payload": mk(T, ld, 4), "n_taken": mk(T, C)}
-        self.buffers = buffers_of(self.t, ld)
+        self.buffers = buffers_of(self.t, ld, n_words, T, C)
 
     @classmethod
     def from_inputs(cls, inp, max_steps=None, device=0):

@@ -120,3 +120,25 @@ def test_valid_descriptor_without_device_is_device_error(lib):
     st, h = rc.rc_cohort_create(**good_desc(), check=False)
     assert st == rc.RC_E_DEVICE
     assert not h.value
+
+
+def plan_lanes_status(lib, d):
+    """rc_plan_lanes on a full descriptor (host only: the same descriptor
+    checks as rc_cohort_create, no device involved)."""
+    off = np.ascontiguousarray(d["cohort_offsets"], dtype=np.uint32)
+    tab = np.ascontiguousarray(d["table"], dtype=np.uint32)
+    cdf = None if d["route_cdf"] is None else np.ascontiguousarray(d["route_cdf"], dtype=np.uint32)
+    desc = rc.RcCohortDesc(d["n_sessions"], d["n_words"], d["n_routes"], off.size - 1,
+                           off.ctypes.data_as(rc._P32), tab.ctypes.data_as(rc._P32),
+                           d["route_mode"], None if cdf is None else cdf.ctypes.data_as(rc._P32),
+                           d["decide_thr"])
+    n = ctypes.c_uint32()
+    return lib.rc_plan_lanes(ctypes.byref(desc), 256, None, None, 0, ctypes.byref(n))
+
+
+@pytest.mark.parametrize("name", sorted(BAD))
+def test_invalid_descriptor_rejected_by_plan_inspection(lib, name):
+    d = good_desc()
+    d.update(BAD[name])
+    assert plan_lanes_status(lib, d) == rc.RC_E_INVALID
+    assert plan_lanes_status(lib, good_desc()) == rc.RC_OK

@@ -109,3 +109,47 @@ def test_two_handles_two_streams_two_threads(orc, mode):
         torch.cuda.synchronize()
         for j in jobs:
             j["co"].close()
+
+
+def advanced(b: "rc.RcBuffers", ld: int, t: int, n_cohorts: int) -> "rc.RcBuffers":
+    """The buffers of b with the effect log and counts advanced by t slices
+    (the pointers a caller passes to continue a chain in the same log)."""
+    return rc.RcBuffers(b.state, b.outcome, b.eff_sid + 4 * t * ld, b.eff_tool + 4 * t * ld,
+                        b.eff_payload + 16 * t * ld, b.n_taken + 4 * t * n_cohorts, ld)
+
+
+def one_handle_two_streams(orc, entry):
+    """A chain continued on another stream by the same handle, with no
+    synchronization by the caller: the second host-round-trip call must wait
+    for the first call's last body kernels (its scratch and the state they
+    write), so the two calls equal one chain of T1 + T2 steps."""
+    import torch
+    W, R, thr, T1, T2 = 32, 64, 19661, 5, 4
+    sizes = [256] * 30 + [100, 64, 17]
+    inp = wk.make_custom(n_words=W, n_routes=R, route_mode=wk.ROUTE_CDF, decide_thr=thr,
+                         cohort_sizes=sizes, n_steps=T1 + T2, seed_key=33_100, ld=sum(sizes) + 64)
+    say("one handle, two streams (%s): N=%d T=%d+%d" % (entry, inp.n_sessions, T1, T2))
+    want = orc.run_inputs(inp, n_steps=T1 + T2)
+    co = rc.Cohort.from_inputs(inp, max_steps=T1 + T2)
+    fn = getattr(rc, "rc_cohort_" + entry)
+    try:
+        torch.cuda.synchronize()
+        sa, sb = torch.cuda.Stream(device=co.device), torch.cuda.Stream(device=co.device)
+        for rep in range(3):
+            co.upload(inp.state, inp.outcome)
+            torch.cuda.synchronize()
+            fn(co.handle, co.buffers, 0, T1, rc.RC_MODE_HOST_ROUNDTRIP, 0, co.n_cohorts,
+               sa.cuda_stream)
+            fn(co.handle, advanced(co.buffers, co.ld, T1, co.n_cohorts), T1, T2,
+               rc.RC_MODE_HOST_ROUNDTRIP, 0, co.n_cohorts, sb.cuda_stream)
+            sb.synchronize()
+            got = co.download(T1 + T2)
+            for k in KEYS:
+                assert np.array_equal(got[k], want[k]), (entry, rep, k)
+    finally:
+        torch.cuda.synchronize()
+        co.close()
+
+
+def test_one_handle_host_round_trip_on_two_streams(orc):
+    one_handle_two_streams(orc, "run_chain")
