@@ -73,6 +73,7 @@ enum rc_chain_mode {
 #define RC_MAX_ROUTES 1024u
 #define RC_MAX_COHORT 256u
 #define RC_MAX_SESSIONS (1u << 28)
+#define RC_NOALLOC_MAX_SESSIONS (1u << 20) /* rc_cohort_run_chain_noalloc */
 
 /*
  * Problem description (the paper's problem statement: sessions with typed
@@ -197,6 +198,29 @@ int rc_cohort_run_chain(rc_cohort *h, const rc_buffers *b, uint32_t step0,
 int rc_cohort_run_floor(rc_cohort *h, const rc_buffers *b, const uint32_t *decisions,
                         uint32_t n_steps, uint32_t cohort_begin, uint32_t cohort_end,
                         void *hip_stream);
+
+/*
+ * For callers that cannot allocate device memory while they run: code being
+ * captured into a HIP graph, tight serving loops, harnesses that forbid
+ * hipMalloc.  Exactly rc_cohort_run_chain (same arguments, same outputs),
+ * except that in RC_MODE_HOST_ROUNDTRIP the per-step scratch -- the
+ * permutation of the stepped sessions and the two counter words -- lives in
+ * one fixed array of device memory of the library (4 MiB plus 256 bytes per
+ * device, held until the process ends) instead of the handle's buffers, and
+ * the counter words are cleared by a kernel launch (no memset) at the start
+ * of every call.  The call allocates nothing: no hipMalloc, hipFree or
+ * allocating library routine (RC_MODE_RESIDENT never uses scratch).  All
+ * host-round-trip calls of this entry point on one device share the array:
+ * each waits on its stream for the previous one (an event recorded after its
+ * last body kernel), which orders calls made from one host thread; calls
+ * made from several host threads at once race.
+ * Errors: those of rc_cohort_run_chain, and RC_E_INVALID (before anything is
+ * enqueued) when the stepped cohorts hold more than RC_NOALLOC_MAX_SESSIONS
+ * sessions.
+ */
+int rc_cohort_run_chain_noalloc(rc_cohort *h, const rc_buffers *b, uint32_t step0,
+                                uint32_t n_steps, int mode, uint32_t cohort_begin,
+                                uint32_t cohort_end, void *hip_stream);
 
 /* Release the handle's device and host resources.  Waits for nothing: the
  * caller synchronizes its streams first.  rc_cohort_destroy(NULL) is RC_OK. */

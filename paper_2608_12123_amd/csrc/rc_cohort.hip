@@ -65,6 +65,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <type_traits>
 #include <vector>
@@ -1535,6 +1536,12 @@ __global__ __launch_bounds__(64) void rc_clear_kernel(uint32_t* p, uint32_t n) {
     if (i < n) p[i] = 0u;
 }
 
+// Scratch of rc_cohort_run_chain_noalloc: two counter words, padding, then
+// the slot-to-session permutation of at most RC_NOALLOC_MAX_SESSIONS
+// sessions.  Each device holds its own copy for the life of the process.
+constexpr uint32_t NOALLOC_PERM_OFF = 64u;
+__device__ __align__(256) uint32_t rc_noalloc_scratch[NOALLOC_PERM_OFF + RC_NOALLOC_MAX_SESSIONS];
+
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
@@ -1703,6 +1710,34 @@ void free_handle(rc_cohort* h) {
     delete h;
 }
 
+// Per device: the address of rc_noalloc_scratch (resolved once, with the
+// device current) and the event that orders the no-allocation
+// host-round-trip calls that share it.
+constexpr int MAX_DEVICES = 64;
+std::mutex g_noalloc_mu;
+uint32_t* g_noalloc_ptr[MAX_DEVICES] = {};
+hipEvent_t g_noalloc_done[MAX_DEVICES] = {};
+bool g_noalloc_pending[MAX_DEVICES] = {};
+
+// Called by rc_cohort_create with `dev` current.
+int noalloc_init(int dev) {
+    if (dev < 0 || dev >= MAX_DEVICES) return RC_E_DEVICE;
+    std::lock_guard<std::mutex> lk(g_noalloc_mu);
+    if (g_noalloc_ptr[dev]) return RC_OK;
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(rc_noalloc_scratch)) != hipSuccess || !ptr) {
+        (void)hipGetLastError();
+        return RC_E_DEVICE;
+    }
+    hipEvent_t ev = nullptr;
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) {
+        (void)hipGetLastError();
+        return RC_E_DEVICE;
+    }
+    g_noalloc_done[dev] = ev;
+    g_noalloc_ptr[dev] = static_cast<uint32_t*>(ptr);
+    return RC_OK;
+}
 
 template <typename T>
 int dev_upload(T** dst, const void* src, size_t bytes) {
@@ -2035,6 +2070,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     if (rc == RC_OK && hipMemset(h->d_ctr, 0, 2 * sizeof(uint32_t)) != hipSuccess) rc = RC_E_DEVICE;
     if (rc == RC_OK && hipHostMalloc((void**)&h->h_word, sizeof(uint32_t), hipHostMallocDefault) != hipSuccess) rc = RC_E_NOMEM;
     if (rc == RC_OK && hipEventCreateWithFlags(&h->hrt_done, hipEventDisableTiming) != hipSuccess) rc = RC_E_DEVICE;
+    if (rc == RC_OK) rc = noalloc_init(hip_device);
     if (rc == RC_OK) {
         ImageArgs ia;
         ia.raw = h->d_raw;
@@ -2093,6 +2129,30 @@ int rc_cohort_run_chain(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint3
     hipStream_t stream = (hipStream_t)hip_stream;
     if (mode == RC_MODE_RESIDENT) return run_resident(h, b, step0, n_steps, cohort_begin, cohort_end, stream);
     return run_host_roundtrip_handle(h, b, step0, n_steps, cohort_begin, cohort_end, stream);
+}
+
+int rc_cohort_run_chain_noalloc(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t n_steps,
+                                int mode, uint32_t cohort_begin, uint32_t cohort_end, void* hip_stream) {
+    if (!h || !b) return RC_E_INVALID;
+    if (mode != RC_MODE_RESIDENT && mode != RC_MODE_HOST_ROUNDTRIP) return RC_E_INVALID;
+    if (cohort_begin > cohort_end || cohort_end > h->C) return RC_E_INVALID;
+    if (h->offsets[cohort_end] - h->offsets[cohort_begin] > RC_NOALLOC_MAX_SESSIONS) return RC_E_INVALID;
+    DeviceGuard guard(h->device);
+    if (!guard.ok) return RC_E_DEVICE;
+    const int v = validate_buffers(h, b, n_steps);
+    if (v != RC_OK) return v;
+    h->last_launches = 0;
+    h->last_d2h = 0;
+    if (n_steps == 0u || cohort_begin == cohort_end) return RC_OK;
+    hipStream_t stream = (hipStream_t)hip_stream;
+    // the resident chain uses no scratch
+    if (mode == RC_MODE_RESIDENT) return run_resident(h, b, step0, n_steps, cohort_begin, cohort_end, stream);
+    uint32_t* base = g_noalloc_ptr[h->device];  // resolved by rc_cohort_create
+    if (!base) return RC_E_DEVICE;
+    uint32_t parity = 0;
+    HrtScratch sc{base + NOALLOC_PERM_OFF, base, &parity, g_noalloc_done[h->device],
+                  &g_noalloc_pending[h->device], true};
+    return run_host_roundtrip(h, b, step0, n_steps, cohort_begin, cohort_end, stream, sc);
 }
 
 int rc_cohort_run_floor(rc_cohort* h, const rc_buffers* b, const uint32_t* decisions, uint32_t n_steps,

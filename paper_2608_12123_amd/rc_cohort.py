@@ -30,9 +30,11 @@ RC_MIN_WORDS, RC_MAX_WORDS = 4, 64
 RC_MAX_ROUTES = 1024
 RC_MAX_COHORT = 256
 RC_MAX_SESSIONS = 1 << 28
+RC_NOALLOC_MAX_SESSIONS = 1 << 20
 
 EXPORTED = [
     "rc_cohort_create", "rc_cohort_step", "rc_cohort_run_chain", "rc_cohort_run_floor",
+    "rc_cohort_run_chain_noalloc",
     "rc_cohort_destroy", "rc_status_string", "rc_cohort_last_counts", "rc_cohort_plan_info",
     "rc_plan_lanes", "rc_pack_shares", "rc_online_compact", "rc_cohorts_from_batches",
 ]
@@ -131,6 +133,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                                         ctypes.c_void_p]
     lib.rc_cohort_run_floor.restype = ctypes.c_int
+    lib.rc_cohort_run_chain_noalloc.argtypes = lib.rc_cohort_run_chain.argtypes
+    lib.rc_cohort_run_chain_noalloc.restype = ctypes.c_int
     lib.rc_cohort_destroy.argtypes = [ctypes.c_void_p]
     lib.rc_cohort_destroy.restype = ctypes.c_int
     lib.rc_cohort_last_counts.argtypes = [ctypes.c_void_p, _P32, _P32]
@@ -223,6 +227,19 @@ def rc_cohort_run_chain(h, buffers: RcBuffers, step0: int, n_steps: int, mode: i
                                             _stream_handle(stream))
     if check:
         _check(st, "rc_cohort_run_chain")
+    return st
+
+
+def rc_cohort_run_chain_noalloc(h, buffers: RcBuffers, step0: int, n_steps: int, mode: int,
+                                cohort_begin: int, cohort_end: int, stream=None,
+                                check: bool = True) -> int:
+    """rc_cohort_run_chain with the host round trip's scratch in the
+    library's fixed device array (no device allocation by the call)."""
+    st = load_library().rc_cohort_run_chain_noalloc(h, ctypes.byref(buffers), step0 & 0xFFFFFFFF,
+                                                    n_steps, mode, cohort_begin, cohort_end,
+                                                    _stream_handle(stream))
+    if check:
+        _check(st, "rc_cohort_run_chain_noalloc")
     return st
 
 
@@ -433,6 +450,13 @@ class Cohort:
         ce = self.n_cohorts if cohort_end is None else cohort_end
         return rc_cohort_run_chain(self.handle, self.buffers, step0, n_steps, mode, cohort_begin,
                                    ce, stream)
+
+    def run_chain_noalloc(self, step0, n_steps, mode=RC_MODE_RESIDENT, cohort_begin=0,
+                          cohort_end=None, stream=None):
+        assert n_steps <= self.max_steps
+        ce = self.n_cohorts if cohort_end is None else cohort_end
+        return rc_cohort_run_chain_noalloc(self.handle, self.buffers, step0, n_steps, mode,
+                                           cohort_begin, ce, stream)
 
     def run_floor(self, decisions: np.ndarray, n_steps, cohort_begin=0, cohort_end=None,
                   stream=None):

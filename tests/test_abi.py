@@ -59,6 +59,7 @@ def test_null_handles(lib):
     assert lib.rc_cohort_destroy(None) == rc.RC_OK
     assert lib.rc_cohort_run_chain(None, None, 0, 1, 0, 0, 1, None) == rc.RC_E_INVALID
     assert lib.rc_cohort_step(None, None, 0, 0, 1, None) == rc.RC_E_INVALID
+    assert lib.rc_cohort_run_chain_noalloc(None, None, 0, 1, 1, 0, 1, None) == rc.RC_E_INVALID
     assert lib.rc_cohort_last_counts(None, None, None) == rc.RC_E_INVALID
     assert lib.rc_cohort_plan_info(None, None, None, None) == rc.RC_E_INVALID
 
