@@ -9,14 +9,19 @@ It prints ONE JSON line with the contract fields plus:
 * ``roofline``: algorithmic bytes per launch of the resident chain kernel
   over its average duration, timed with HIP events on the launch stream,
   with the HBM traffic of the committed rocprofv3 counter summary;
+  ``roofline_by_workload`` gives the same block (with its VALU busy
+  fraction) for each single-launch workload: 100,000 and 1,000,000 sessions;
 * ``valu``: VALU instructions per launch (committed SQ counter summary) and
   the fraction of the chip's VALU issue they occupy;
 * ``host_roundtrip``: the same workload through the host-round-trip
   mechanism (4-byte readback + host branch + relaunch every chained step);
 * ``floor``: the no-decision floor (decisions replayed from a bitmap);
 * ``mechanisms``: resident, synchronized resident, floor and host round trip
-  on all five workloads (median of timed rows: microseconds per invocation
-  and per chained step, launches and device-to-host copies per invocation);
+  on all five workloads with the paper's row protocol (5 warmups, 3
+  calibration samples, 30 rows of at least 100 ms each; median row in
+  microseconds per invocation and per chained step, launches and
+  device-to-host copies per invocation), beside the paper's own resident
+  and host-round-trip medians (``mechanisms_paper_context``);
 * ``cpu_baseline``: the single-threaded CPU oracle on the same workload, and
   the safe-suffix threshold K_r (batch sizes and chain lengths where the
   resident chain beats the oracle on one core and on all cores);
@@ -28,6 +33,13 @@ It prints ONE JSON line with the contract fields plus:
 Inputs are synthetic and seeded (see paper_2608_12123_amd/workload.py).  The
 timed region rotates through enough buffer sets that the working set is
 larger than the 256 MB Infinity Cache.
+
+Profiling modes: ``--profile-only`` (just the timed resident loop, for
+counter runs), ``--copy-calibration`` (a plain copy of known size, the HBM
+counter scale), ``--trace-mechanisms`` (resident and host-round-trip
+invocation blocks on every workload, for a rocprofv3 kernel and memory-copy
+trace) and ``--summarize-trace DIR PLAN`` (launches and device-to-host
+copies per invocation from such a trace).
 """
 from __future__ import annotations
 
@@ -253,22 +265,56 @@ def time_hrt(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
     return time.perf_counter() - t0
 
 
-MECH_ROWS = 9  # timed rows per mechanism and workload (median reported)
+# The paper's row protocol (Section 7 "Grid and independent unit"): per
+# workload and mechanism, 5 warmup invocations, 3 calibration samples, then
+# 30 timed rows of at least 100 ms of work each; the median row is reported.
+MECH_WARMUPS = 5
+MECH_CALIBRATION = 3
+MECH_ROWS = 30
+MECH_ROW_S = 0.100
 
 
-def _rows(timed, n_per_row, rows=MECH_ROWS):
-    """Microseconds per invocation of `rows` timed rows of n_per_row
-    invocations each: (median, 10th percentile, 90th percentile)."""
-    us = [timed(n_per_row) / n_per_row * 1e6 for _ in range(rows)]
-    return float(np.median(us)), float(np.percentile(us, 10)), float(np.percentile(us, 90))
+def _calibrated_count(timed, row_s, first=10, min_sample_s=0.02):
+    """Invocations per row so that a row takes at least row_s: the median
+    per-invocation time of MECH_CALIBRATION samples, each grown until it
+    takes at least min_sample_s, plus a 10% margin."""
+    k = first
+    while True:
+        t = timed(k)
+        if t >= min_sample_s or k >= 1 << 20:
+            break
+        k = int(k * max(2.0, 1.2 * min_sample_s / max(t, 1e-9)))
+    per = float(np.median([t / k] + [timed(k) / k for _ in range(MECH_CALIBRATION - 1)]))
+    return max(1, int(np.ceil(1.1 * row_s / max(per, 1e-9)))), per
 
 
-def mechanism_row(rc, wk, key, budget_s=1.0):
+def _rows(timed, n_per_row, rows, row_s=0.0):
+    """Microseconds per invocation and milliseconds per row of `rows` timed
+    rows of n_per_row invocations each: (median, 10th percentile, 90th
+    percentile, median row ms, invocations per row).  Rows whose median
+    falls short of row_s are timed again with a count scaled up to match."""
+    for _ in range(3):
+        secs = [timed(n_per_row) for _ in range(rows)]
+        med = float(np.median(secs))
+        if med >= row_s:
+            break
+        n_per_row = int(np.ceil(n_per_row * 1.05 * row_s / max(med, 1e-9)))
+    us = [t / n_per_row * 1e6 for t in secs]
+    return (float(np.median(us)), float(np.percentile(us, 10)), float(np.percentile(us, 90)),
+            med * 1e3, n_per_row)
+
+
+def mechanism_row(rc, wk, key, rows=MECH_ROWS, row_s=MECH_ROW_S, common_count=False):
     """Resident (pipelined and synchronized), no-decision floor and host
-    round trip on one workload, invocations as the workload defines them.
-    Protocol: warmups, a calibration of the invocation count on the faster
-    (resident) mechanism, then MECH_ROWS timed rows per mechanism; the
-    median row is reported with its 10th-90th percentile spread."""
+    round trip on one workload, invocations as the workload defines them, with
+    the paper's row protocol.  Each mechanism's row count is calibrated on
+    that mechanism so that every row holds at least row_s of its work; with
+    common_count, every mechanism uses the count calibrated on the fastest
+    one (the pipelined resident chain), as in the paper -- whose mechanisms
+    differ by at most 2.4x, while here the host round trip is 4-42x slower,
+    which makes its rows that much longer.  Single-launch workloads rotate
+    enough buffer sets that a row streams from HBM, not from the 256 MB
+    Infinity Cache."""
     import torch
     wl = wk.WORKLOADS[key]
     inp = wk.make_inputs(wl)
@@ -281,53 +327,67 @@ def mechanism_row(rc, wk, key, budget_s=1.0):
         if wl.per_cohort_invocation:
             ranges = [(c, c + 1) for c in range(inp.n_cohorts)]
             per_inv = wl.cohort_size * T
+            n_sets = 1
         else:
             ranges = [(0, inp.n_cohorts)]
             per_inv = inp.n_sessions * T
-        sets = Sets(rc, inp, T, 1 if wl.per_cohort_invocation else 2)
+            probe = Sets(rc, inp, T, 1)
+            n_sets = n_sets_for(probe.bytes_per_set())
+            del probe
+        sets = Sets(rc, inp, T, n_sets)
         stream = torch.cuda.current_stream().cuda_stream
-        # warm up, then calibrate the invocations per row on the resident mechanism
-        w, _ = time_resident(rc, h, sets, inp, T, 20, 5, stream, ranges)
-        n = int(max(10, min(20000, budget_s / 4 / MECH_ROWS / max(w / 20, 1e-7))))
-        r_med, r_lo, r_hi = _rows(lambda k: time_resident(rc, h, sets, inp, T, k, 0, stream, ranges)[0], n)
+        bits = floor_bits(rc, h, inp, T, stream)
+        timers = {
+            "resident": lambda k: time_resident(rc, h, sets, inp, T, k, 0, stream, ranges)[0],
+            "resident_synced": lambda k: time_resident_synced(rc, h, sets, inp, T, k, stream, ranges),
+            "floor": lambda k: time_floor(rc, h, sets, bits, inp, T, k, 0, stream, ranges),
+            "host_rt": lambda k: time_hrt(rc, h, sets, inp, T, k, 0, stream, ranges),
+        }
+        res = {}
+        counts = {}
+        for name, timed in timers.items():
+            timed(MECH_WARMUPS)
+            n, _ = _calibrated_count(timed, row_s)
+            counts[name] = n
+        if common_count:
+            counts = {name: counts["resident"] for name in counts}
+        for name, timed in timers.items():
+            res[name] = _rows(timed, counts[name], rows, 0.0 if common_count else row_s)
+            counts[name] = res[name][4]
         rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_RESIDENT, *ranges[0], stream)
         res_counts = rc.rc_cohort_last_counts(h)
-        n_sync = max(5, n // 4)
-        s_med, s_lo, s_hi = _rows(lambda k: time_resident_synced(rc, h, sets, inp, T, k, stream, ranges),
-                                  n_sync)
-        bits = floor_bits(rc, h, inp, T, stream)
-        time_floor(rc, h, sets, bits, inp, T, 5, 5, stream, ranges)
-        f_med, f_lo, f_hi = _rows(lambda k: time_floor(rc, h, sets, bits, inp, T, k, 0, stream, ranges), n)
-        w1 = time_hrt(rc, h, sets, inp, T, 3, 1, stream, ranges)
-        n_h = int(max(3, min(n, budget_s / 4 / MECH_ROWS / max(w1 / 3, 1e-7))))
-        h_med, h_lo, h_hi = _rows(lambda k: time_hrt(rc, h, sets, inp, T, k, 0, stream, ranges), n_h)
         rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, *ranges[0], stream)
         hrt_counts = rc.rc_cohort_last_counts(h)
         torch.cuda.synchronize()
+        set_bytes = sets.bytes_per_set()
     finally:
         rc.rc_cohort_destroy(h)
-    spread = lambda lo, hi: [round(lo, 3), round(hi, 3)]
+    spread = lambda x: [round(x[1], 3), round(x[2], 3)]
+    r_med, s_med, f_med, h_med = (res[k][0] for k in ("resident", "resident_synced", "floor", "host_rt"))
     return {
         "workload": wl.title, "T": T, "transitions_per_invocation": per_inv,
         "resident_us_per_invocation": round(r_med, 3),
-        "resident_us_p10_p90": spread(r_lo, r_hi),
+        "resident_us_p10_p90": spread(res["resident"]),
         "resident_us_per_chained_step": round(r_med / T, 4),
         "resident_synced_us_per_invocation": round(s_med, 3),
-        "resident_synced_us_p10_p90": spread(s_lo, s_hi),
+        "resident_synced_us_p10_p90": spread(res["resident_synced"]),
         "host_rt_us_per_invocation": round(h_med, 3),
-        "host_rt_us_p10_p90": spread(h_lo, h_hi),
+        "host_rt_us_p10_p90": spread(res["host_rt"]),
         "host_rt_us_per_chained_step": round(h_med / T, 4),
         "host_over_resident": round(h_med / r_med, 3),
         "host_over_resident_synced": round(h_med / s_med, 3),
         "floor_us_per_invocation": round(f_med, 3),
-        "floor_us_p10_p90": spread(f_lo, f_hi),
+        "floor_us_p10_p90": spread(res["floor"]),
         "resident_over_floor": round(r_med / f_med, 3),
         "resident_transitions_per_s": round(per_inv / (r_med * 1e-6), 1),
         "host_rt_transitions_per_s": round(per_inv / (h_med * 1e-6), 1),
         "launches_per_invocation": {"resident": res_counts[0], "host_rt": hrt_counts[0]},
         "d2h_copies_per_invocation": {"resident": res_counts[1], "host_rt": hrt_counts[1]},
-        "invocations_per_row": {"resident": n, "resident_synced": n_sync, "host_rt": n_h, "floor": n},
-        "rows": MECH_ROWS,
+        "invocations_per_row": counts,
+        "row_ms": {k: round(v[3], 2) for k, v in res.items()},
+        "rows": rows, "warmups": MECH_WARMUPS, "calibration_samples": MECH_CALIBRATION,
+        "common_count": common_count,
+        "buffer_sets_rotated": n_sets, "bytes_per_buffer_set": set_bytes,
     }
 
 
@@ -359,6 +419,41 @@ def hbm_measured(n_bytes=512 << 20, reps=10):
     return out
 
 
+def cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), else what platform
+    reports."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+# The paper's primary mechanism cell (Section 8 "Mechanism results", primary
+# table): median over 30 rows of the batch-average wall time of one 32-epoch
+# invocation (N = 256 agents, H = 32 chained epochs), one global decision
+# per epoch over a 16-byte state, CUDA graphs, four NVIDIA placements.
+PAPER_CONTEXT = {
+    "what": "the paper's primary cell (N=256 agents, H=32 chained epochs, one global decision per "
+            "epoch, 16-byte state, CUDA-graph mechanisms): median row us per 32-epoch invocation",
+    "rows": [
+        {"placement": "GTX 1660 Ti (local)", "resident_us": 273.0, "host_rt_us": 467.2,
+         "host_over_resident": 1.71, "floor_us": 33.4},
+        {"placement": "L4 (Modal)", "resident_us": 261.9, "host_rt_us": 625.3,
+         "host_over_resident": 2.39, "floor_us": 39.7},
+        {"placement": "L4 (RunPod)", "resident_us": 258.3, "host_rt_us": 533.3,
+         "host_over_resident": 2.06, "floor_us": 37.3},
+        {"placement": "H100 SXM5 (Lambda)", "resident_us": 309.0, "host_rt_us": 567.5,
+         "host_over_resident": 1.84, "floor_us": 45.6},
+    ],
+    "ratio_range_all_cells": [1.19, 2.39],
+    "note": "a different mechanism and hardware: context only, not a target",
+}
+
+
 def cpu_baseline(inp, T, min_seconds):
     """The oracle (plain single-threaded C) on the same workload, repeated
     until at least ``min_seconds`` of CPU work; also returns its outputs of
@@ -379,8 +474,8 @@ def cpu_baseline(inp, T, min_seconds):
     return {"value": round(trans / el, 1), "unit": "transitions/s", "cores": 1, "kind": "oracle",
             "sample": "full workload (%d sessions x %d chained steps), %d repetition(s), %.1f s, "
                       "single thread, gcc -O2; host %s, %d logical CPUs"
-                      % (inp.n_sessions, T, reps, el, platform.processor() or platform.machine(),
-                         os.cpu_count() or 0)}, first
+                      % (inp.n_sessions, T, reps, el, cpu_model(), os.cpu_count() or 0),
+            "cpu_model": cpu_model(), "host_logical_cpus": os.cpu_count() or 0}, first
 
 
 def oracle_call_times(orc, inp, T, seconds, n_threads=1):
@@ -571,6 +666,173 @@ def cohort_former(rc, wk, latency_ns, ks=(32, 64, 128, 256), reps=3, seeds=(0, 1
             "by_K": rows}
 
 
+def valu_of(key, k_avg_ms):
+    """VALU instructions per launch of the workload's chain kernel (committed
+    SQ counter summary) and the fraction of the chip's VALU issue they
+    occupy over the measured kernel time; None when the summary is stale."""
+    valu = stored_valu(key)
+    if valu is None:
+        return None
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    busy = valu["insts_per_launch"] * 4.0 / (4 * cus * ENGINE_CLOCK_HZ * k_avg_ms * 1e-3)
+    return {"insts_per_launch": valu["insts_per_launch"],
+            "insts_per_wave": round(valu["insts_per_launch"] / valu["waves"], 1),
+            "busy_frac": round(busy, 4),
+            "basis": "SQ_INSTS_VALU (committed rocprofv3 summary) x 4 cycles / "
+                     "(4 SIMDs x CUs x 2.4 GHz x measured kernel time)"}
+
+
+def roofline_of(key, inp, T, k_avg_ms):
+    """The HBM roofline block of one workload's resident chain kernel:
+    algorithmic bytes per launch over the event-timed average launch."""
+    abytes = algorithmic_bytes(inp.n_sessions, inp.n_words, T, inp.n_cohorts)
+    achieved = abytes / (k_avg_ms * 1e-3) / 1e9
+    traffic = stored_traffic(key)
+    blk = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+           "kernel": "rc_chain_kernel", "algorithmic_bytes_per_launch": abytes,
+           "kernel_us": round(k_avg_ms * 1e3, 3)}
+    if traffic is not None:
+        blk["traffic_over_algorithmic"] = round(traffic / abytes, 4)
+    valu = valu_of(key, k_avg_ms)
+    if valu is not None:
+        blk["valu"] = valu
+    return blk
+
+
+def measure_roofline(rc, wk, key, steps, warmup):
+    """Time `steps` resident launches of a single-launch workload (rotating
+    buffer sets larger than the Infinity Cache) and return its roofline block."""
+    import torch
+    wl = wk.WORKLOADS[key]
+    inp = wk.make_inputs(wl)
+    T = wl.n_steps
+    h = rc.rc_cohort_create(n_sessions=inp.n_sessions, n_words=inp.n_words, n_routes=inp.n_routes,
+                            cohort_offsets=inp.cohort_offsets, table=inp.table,
+                            route_mode=inp.route_mode, route_cdf=inp.route_cdf,
+                            decide_thr=inp.decide_thr)
+    try:
+        probe = Sets(rc, inp, T, 1)
+        n_sets = n_sets_for(probe.bytes_per_set())
+        del probe
+        sets = Sets(rc, inp, T, n_sets)
+        stream = torch.cuda.current_stream().cuda_stream
+        _, region_ms = time_resident(rc, h, sets, inp, T, steps, warmup, stream)
+        blk = roofline_of(key, inp, T, region_ms / steps)
+        blk.update({"workload": wl.title, "launches_timed": steps, "buffer_sets_rotated": n_sets})
+        return blk
+    finally:
+        torch.cuda.synchronize()
+        rc.rc_cohort_destroy(h)
+
+
+TRACE_GAP_S = 0.2  # idle time between the blocks of --trace-mechanisms
+
+
+def trace_mechanisms(rc, wk, n=20):
+    """For a kernel and memory-copy trace (rocprofv3): on every workload, n
+    resident invocations, then n host-round-trip invocations, each block
+    followed by TRACE_GAP_S of idle time so that --summarize-trace can cut
+    the trace into blocks.  Prints the block plan as one JSON line."""
+    import torch
+    blocks = []
+    stream = torch.cuda.current_stream().cuda_stream
+    for key in wk.WORKLOAD_ORDER:
+        wl = wk.WORKLOADS[key]
+        inp = wk.make_inputs(wl)
+        T = wl.n_steps
+        h = rc.rc_cohort_create(n_sessions=inp.n_sessions, n_words=inp.n_words, n_routes=inp.n_routes,
+                                cohort_offsets=inp.cohort_offsets, table=inp.table,
+                                route_mode=inp.route_mode, route_cdf=inp.route_cdf,
+                                decide_thr=inp.decide_thr)
+        try:
+            sets = Sets(rc, inp, T, 1)
+            ranges = ([(c, c + 1) for c in range(inp.n_cohorts)] if wl.per_cohort_invocation
+                      else [(0, inp.n_cohorts)])
+            torch.cuda.synchronize()
+            time.sleep(TRACE_GAP_S)
+            for mech, mode in (("resident", rc.RC_MODE_RESIDENT), ("host_rt", rc.RC_MODE_HOST_ROUNDTRIP)):
+                for i in range(n):
+                    cb, ce = ranges[i % len(ranges)]
+                    rc.rc_cohort_run_chain(h, sets[0], 0, T, mode, cb, ce, stream)
+                counts = rc.rc_cohort_last_counts(h)
+                torch.cuda.synchronize()
+                time.sleep(TRACE_GAP_S)
+                blocks.append({"workload": key, "mechanism": mech, "invocations": n, "T": T,
+                               "library_counts_per_invocation": list(counts)})
+        finally:
+            rc.rc_cohort_destroy(h)
+    print(json.dumps({"trace_blocks": blocks, "gap_s": TRACE_GAP_S}), flush=True)
+
+
+def summarize_trace(trace_dir, plan_path):
+    """Launches and device-to-host copies per invocation from a rocprofv3
+    trace (--kernel-trace --hip-trace --memory-copy-trace) of
+    --trace-mechanisms.  The library's chain-step kernels (chain, decide,
+    body, counter clear) are cut into blocks at idle gaps longer than half of
+    TRACE_GAP_S; in each block's time window (from half a gap before its first
+    kernel to a quarter gap after its last) it counts the runtime's copy
+    kernels (small device-to-host copies into pinned memory run as
+    __amd_rocclr_copyBuffer), the hipMemcpy* calls of the HIP API trace and
+    the SDMA device-to-host copies of the memory-copy trace.  Prints a
+    markdown table."""
+    import csv
+    import glob
+
+    def rows(pattern):
+        out = []
+        for path in sorted(glob.glob(os.path.join(trace_dir, "**", pattern), recursive=True)):
+            out.extend(csv.DictReader(open(path)))
+        return out
+
+    plan = None
+    with open(plan_path) as f:
+        for line in f:
+            if line.startswith("{") and "trace_blocks" in line:
+                plan = json.loads(line)
+    lib_kernels = ("rc_chain_kernel", "rc_decide_kernel", "rc_body_kernel", "rc_clear_kernel")
+    ev, blit = [], []
+    for r in rows("*kernel_trace.csv"):
+        name = r.get("Kernel_Name", "")
+        t0, t1 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+        if any(k in name for k in lib_kernels):
+            ev.append((t0, t1, name))
+        elif "copyBuffer" in name:
+            blit.append(t0)
+    ev.sort()
+    api = [int(r["Start_Timestamp"]) for r in rows("*hip_api_trace.csv")
+           if r.get("Function", "").startswith("hipMemcpy")]
+    sdma = [int(r["Start_Timestamp"]) for r in rows("*memory_copy_trace.csv")
+            if "DEVICE_TO_HOST" in r.get("Direction", "")]
+    gap_ns = plan["gap_s"] * 1e9
+    segs = []
+    for e in ev:
+        if segs and e[0] - segs[-1]["end"] < gap_ns / 2:
+            segs[-1]["ev"].append(e)
+            segs[-1]["end"] = max(segs[-1]["end"], e[1])
+        else:
+            segs.append({"start": e[0], "end": e[1], "ev": [e]})
+    blocks = plan["trace_blocks"]
+    if len(segs) != len(blocks):
+        raise SystemExit("trace has %d kernel blocks, the plan %d" % (len(segs), len(blocks)))
+    lines = ["| Workload | Mechanism | Invocations | Library kernel dispatches | Copy-kernel dispatches "
+             "| hipMemcpy calls | SDMA D2H copies | Library's own counts (launches, D2H) "
+             "| Mean chain-kernel us |", "|---|---|---|---|---|---|---|---|---|"]
+    for seg, b in zip(segs, blocks):
+        n = b["invocations"]
+        lo, hi = seg["start"] - gap_ns / 2, seg["end"] + gap_ns / 4
+        inside = lambda ts: sum(1 for t in ts if lo <= t <= hi) / n
+        chain = [e[1] - e[0] for e in seg["ev"] if "rc_chain_kernel" in e[2]]
+        lines.append("| %s | %s | %d | %.2f | %.2f | %.2f | %.2f | %s | %s |" % (
+            b["workload"], b["mechanism"], n, len(seg["ev"]) / n, inside(blit), inside(api),
+            inside(sdma), tuple(b["library_counts_per_invocation"]),
+            "%.2f" % (sum(chain) / len(chain) / 1e3) if chain else "-"))
+    lines.append("")
+    lines.append("Per invocation (counts divided by the block's invocations).")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -588,7 +850,22 @@ def main():
                     help="only the resident timed loop (for rocprofv3 counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only a plain device-to-device copy of known size (HBM counter scale)")
+    ap.add_argument("--roofline-workloads", default="s100k,s1m",
+                    help="single-launch workloads given a roofline block beside the headline")
+    ap.add_argument("--mech-rows", type=int, default=MECH_ROWS)
+    ap.add_argument("--mech-row-ms", type=float, default=MECH_ROW_S * 1e3)
+    ap.add_argument("--mech-common-count", action="store_true",
+                    help="one invocation count per workload for every mechanism, calibrated on the "
+                         "fastest (the paper's protocol; the host-round-trip rows get long)")
+    ap.add_argument("--trace-mechanisms", action="store_true",
+                    help="only the block sequence for a kernel + memory-copy trace (rocprofv3)")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_DIR", "PLAN_OUTPUT"),
+                    help="summarize a rocprofv3 trace of --trace-mechanisms and exit")
     args = ap.parse_args()
+
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -617,6 +894,9 @@ def main():
     if not torch.cuda.is_available():
         sys.exit("bench.py needs an MI355X: no GPU is visible")
     rc.load_library()
+    if args.trace_mechanisms:
+        trace_mechanisms(rc, wk)
+        return
     wl = wk.WORKLOADS[args.workload]
     inp = wk.make_inputs(wl)
     T = wl.n_steps
@@ -648,9 +928,7 @@ def main():
     value = trans_per_step * args.steps / wall
     ms_per_step = wall / args.steps * 1e3
     k_avg_ms = region_ms / args.steps
-    abytes = algorithmic_bytes(N, W, T, C)
-    achieved = abytes / (k_avg_ms * 1e-3) / 1e9
-    traffic = stored_traffic(wl.key)
+    roof = roofline_of(wl.key, inp, T, k_avg_ms)
     out = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -675,23 +953,20 @@ def main():
         "kernel_us": {"avg": round(k_avg_ms * 1e3, 3),
                       "timing": "one HIP event pair on the launch stream around the timed "
                                 "loop, divided by the launches"},
-        "roofline": {
-            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": traffic,
-            "kernel": "rc_chain_kernel", "algorithmic_bytes_per_launch": abytes,
-        },
+        "roofline": {k: v for k, v in roof.items() if k != "valu"},
         "verified_vs_oracle": verified,
     }
-    valu = stored_valu(wl.key)
-    if valu is not None:
-        cus = torch.cuda.get_device_properties(0).multi_processor_count
-        busy = valu["insts_per_launch"] * 4.0 / (4 * cus * ENGINE_CLOCK_HZ * k_avg_ms * 1e-3)
-        out["valu"] = {"insts_per_launch": valu["insts_per_launch"],
-                       "insts_per_wave": round(valu["insts_per_launch"] / valu["waves"], 1),
-                       "busy_frac": round(busy, 4),
-                       "basis": "SQ_INSTS_VALU (committed rocprofv3 summary) x 4 cycles / "
-                                "(4 SIMDs x CUs x 2.4 GHz x measured kernel time)"}
+    if "valu" in roof:
+        out["valu"] = roof["valu"]
+    by_wl = {}
+    for key in [k for k in args.roofline_workloads.split(",") if k]:
+        if key == wl.key:
+            by_wl[key] = dict(roof, workload=wl.title, launches_timed=args.steps,
+                              buffer_sets_rotated=n_sets)
+        else:
+            by_wl[key] = measure_roofline(rc, wk, key, max(10, min(args.steps, 500)), min(args.warmup, 10))
+    if by_wl:
+        out["roofline_by_workload"] = by_wl
     if not args.profile_only:
         hs = max(5, min(args.hrt_steps, args.steps))
         wall_h = time_hrt(rc, h, sets, inp, T, hs, 3, stream)
@@ -732,7 +1007,9 @@ def main():
                 lat_us = max(r["gpu_us"] for r in kr["rows"] if r["K"] == 256 and r["T"] == 16)
             out["cohort_former"] = cohort_former(rc, wk, int(round(lat_us * 1e3)))
         if not args.no_mechanisms:
-            out["mechanisms"] = {k: mechanism_row(rc, wk, k) for k in wk.WORKLOAD_ORDER}
+            out["mechanisms"] = {k: mechanism_row(rc, wk, k, args.mech_rows, args.mech_row_ms * 1e-3,
+                                                  args.mech_common_count) for k in wk.WORKLOAD_ORDER}
+            out["mechanisms_paper_context"] = PAPER_CONTEXT
     rc.rc_cohort_destroy(h)
     print(json.dumps(out), flush=True)
 
