@@ -114,9 +114,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     missing = [n for n in EXPORTED if not hasattr(lib, n)]
     if missing and (path == os.path.join(PKG, "librc_cohort.so") or set(missing) & set(HOST_ONLY)):
         raise RuntimeError("%s lacks %s" % (path, ", ".join(missing)))
-    if missing:
-        # a host-only build: declare only what it holds
-        _declare_host(lib)
+    _declare_host(lib)
+    if "rc_cohort_create" in missing:
+        # a host-only build (no device entry point)
         _lib = lib
         return lib
     lib.rc_cohort_create.argtypes = [ctypes.POINTER(RcCohortDesc), ctypes.c_int,
@@ -133,15 +133,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                                         ctypes.c_void_p]
     lib.rc_cohort_run_floor.restype = ctypes.c_int
-    lib.rc_cohort_run_chain_noalloc.argtypes = lib.rc_cohort_run_chain.argtypes
-    lib.rc_cohort_run_chain_noalloc.restype = ctypes.c_int
+    if "rc_cohort_run_chain_noalloc" not in missing:
+        lib.rc_cohort_run_chain_noalloc.argtypes = lib.rc_cohort_run_chain.argtypes
+        lib.rc_cohort_run_chain_noalloc.restype = ctypes.c_int
     lib.rc_cohort_destroy.argtypes = [ctypes.c_void_p]
     lib.rc_cohort_destroy.restype = ctypes.c_int
     lib.rc_cohort_last_counts.argtypes = [ctypes.c_void_p, _P32, _P32]
     lib.rc_cohort_last_counts.restype = ctypes.c_int
     lib.rc_cohort_plan_info.argtypes = [ctypes.c_void_p, _P32, _P32, _P32]
     lib.rc_cohort_plan_info.restype = ctypes.c_int
-    _declare_host(lib)
     _lib = lib
     return lib
 
