@@ -845,9 +845,8 @@ struct ChainF {
     // synchronization needed.  A wavefront's stores then cover its
     // sessions' contiguous slots, whole cache lines, and go out
     // nontemporal.  Cohorts spanning wavefronts store each effect directly
-    // at its slot through the L2, which merges the lines that several
-    // wavefronts fill (an LDS exchange across wavefronts at every step
-    // costs more than it saves).
+    // at its slot (an LDS exchange across wavefronts at every step costs
+    // more than it saves).
 
     static __device__ __forceinline__ uint4 lds128(const uint32_t* lds, uint32_t byte_off) {
         return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(lds) + byte_off);
@@ -1105,7 +1104,11 @@ struct ChainF {
                         lds_add[(par + i) * NLA + alane] = add[i];
                     }
                 }
-                __builtin_amdgcn_s_setprio(0);
+                // The two-role split keeps the raised priority through the A
+                // lanes' replay too: their effect stores then start ahead of
+                // the B lanes' bulk update (measured: 100,000 sessions 18.1 ->
+                // 16.9 us together with the nontemporal payloads).
+                if constexpr (!SPLIT || PIPE) __builtin_amdgcn_s_setprio(0);
             }
         };
 
@@ -1203,10 +1206,15 @@ struct ChainF {
                         // the cohort)
                         const bool put = L.active && slot - L.b < L.k;
                         if constexpr (MULTI) {
+                            // a wavefront's taken and not-taken sessions land
+                            // in two contiguous slot runs, so its 16-byte
+                            // payloads fill most lines whole: those go out
+                            // nontemporal; the 4-byte fields, spread over more
+                            // partly filled lines, through the L2
                             if (put) {
                                 st32(p_sid, slot << 2, L.s);
                                 st32(p_tool, slot << 2, tool);
-                                st128(p_pay, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
+                                st128<true>(p_pay, slot << 4, make_uint4(S[0], S[1], S[2], S[3]));
                                 if (in_c == 0u) st32(p_cnt, L.c << 2, n1);
                             }
                         } else {
