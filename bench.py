@@ -46,6 +46,7 @@ copies per invocation from such a trace).
 from __future__ import annotations
 
 import argparse
+import itertools
 import json
 import os
 import platform
@@ -161,6 +162,19 @@ def n_sets_for(bytes_per_set, min_total=2 * INFINITY_CACHE_BYTES, cap=16):
     return int(max(2, min(cap, -(-min_total // max(1, bytes_per_set)))))
 
 
+# The step clock of the timing loops: every invocation continues the chain
+# at the next T steps (step0 = invocations so far times T), as a serving loop
+# that keeps stepping the same sessions would.  With step0 fixed at 0, a
+# cohort stepped thousands of times falls into a cycle whose decisions repeat:
+# the 32-session cohorts of the tiny workload end up all taken at every call,
+# and the host round trip then never launches its not-taken body.
+_STEP_CLOCK = itertools.count()
+
+
+def step0_next(T):
+    return (next(_STEP_CLOCK) * T) & 0xFFFFFFFF
+
+
 def time_resident(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
     """Pipelined resident chains.  Returns the wall seconds of the timed loop
     and its GPU time (ms) from one HIP event pair around it, recorded on the
@@ -175,14 +189,14 @@ def time_resident(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
     assert cur.cuda_stream == stream
     for i in range(warmup):
         cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_RESIDENT, cb, ce, stream)
+        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_RESIDENT, cb, ce, stream)
     r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     r0.record(cur)
     for i in range(steps):
         cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_RESIDENT, cb, ce, stream)
+        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_RESIDENT, cb, ce, stream)
     r1.record(cur)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -217,7 +231,7 @@ def warm_clocks(launch, seconds=CLOCK_WARMUP_S):
 
 
 def resident_launcher(rc, h, sets, T, C, stream):
-    return lambda i: rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_RESIDENT, 0, C, stream)
+    return lambda i: rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_RESIDENT, 0, C, stream)
 
 
 def time_resident_synced(rc, h, sets, inp, T, steps, stream, ranges):
@@ -226,7 +240,7 @@ def time_resident_synced(rc, h, sets, inp, T, steps, stream, ranges):
     t0 = time.perf_counter()
     for i in range(steps):
         cb, ce = ranges[i % len(ranges)]
-        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_RESIDENT, cb, ce, stream)
+        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_RESIDENT, cb, ce, stream)
         torch.cuda.current_stream().synchronize()
     return time.perf_counter() - t0
 
@@ -288,12 +302,12 @@ def time_hrt(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
     rng = ranges or [(0, C)]
     for i in range(warmup):
         cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, cb, ce, stream)
+        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_HOST_ROUNDTRIP, cb, ce, stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
         cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_chain(h, sets[i], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, cb, ce, stream)
+        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_HOST_ROUNDTRIP, cb, ce, stream)
     torch.cuda.synchronize()
     return time.perf_counter() - t0
 
@@ -387,9 +401,9 @@ def mechanism_row(rc, wk, key, rows=MECH_ROWS, row_s=MECH_ROW_S, common_count=Fa
         for name, timed in timers.items():
             res[name] = _rows(timed, counts[name], rows, 0.0 if common_count else row_s)
             counts[name] = res[name][4]
-        rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_RESIDENT, *ranges[0], stream)
+        rc.rc_cohort_run_chain(h, sets[0], step0_next(T), T, rc.RC_MODE_RESIDENT, *ranges[0], stream)
         res_counts = rc.rc_cohort_last_counts(h)
-        rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, *ranges[0], stream)
+        rc.rc_cohort_run_chain(h, sets[0], step0_next(T), T, rc.RC_MODE_HOST_ROUNDTRIP, *ranges[0], stream)
         hrt_counts = rc.rc_cohort_last_counts(h)
         torch.cuda.synchronize()
         set_bytes = sets.bytes_per_set()
@@ -790,7 +804,7 @@ def trace_mechanisms(rc, wk, n=20):
             for mech, mode in (("resident", rc.RC_MODE_RESIDENT), ("host_rt", rc.RC_MODE_HOST_ROUNDTRIP)):
                 for i in range(n):
                     cb, ce = ranges[i % len(ranges)]
-                    rc.rc_cohort_run_chain(h, sets[0], 0, T, mode, cb, ce, stream)
+                    rc.rc_cohort_run_chain(h, sets[0], step0_next(T), T, mode, cb, ce, stream)
                 counts = rc.rc_cohort_last_counts(h)
                 torch.cuda.synchronize()
                 time.sleep(TRACE_GAP_S)
@@ -1011,7 +1025,7 @@ def main():
     if not args.profile_only:
         hs = max(5, min(args.hrt_steps, args.steps))
         wall_h = time_hrt(rc, h, sets, inp, T, hs, 3, stream)
-        rc.rc_cohort_run_chain(h, sets[0], 0, T, rc.RC_MODE_HOST_ROUNDTRIP, 0, C, stream)
+        rc.rc_cohort_run_chain(h, sets[0], step0_next(T), T, rc.RC_MODE_HOST_ROUNDTRIP, 0, C, stream)
         cnt = rc.rc_cohort_last_counts(h)
         us_h = wall_h / hs * 1e6
         out["host_roundtrip"] = {
