@@ -46,7 +46,6 @@ copies per invocation from such a trace).
 from __future__ import annotations
 
 import argparse
-import itertools
 import json
 import os
 import platform
@@ -168,14 +167,67 @@ def n_sets_for(bytes_per_set, min_total=2 * INFINITY_CACHE_BYTES, cap=16):
 # cohort stepped thousands of times falls into a cycle whose decisions repeat:
 # the 32-session cohorts of the tiny workload end up all taken at every call,
 # and the host round trip then never launches its not-taken body.
-_STEP_CLOCK = itertools.count()
+_STEP_CLOCK = [0]
+
+
+def step_block(n):
+    """Reserve n invocations on the step clock; returns the first one."""
+    first = _STEP_CLOCK[0]
+    _STEP_CLOCK[0] += n
+    return first
 
 
 def step0_next(T):
-    return (next(_STEP_CLOCK) * T) & 0xFFFFFFFF
+    return (step_block(1) * T) & 0xFFFFFFFF
 
 
-def time_resident(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
+class Launches:
+    """Pre-bound calls of one handle for the timing loops.  Invocation i uses
+    buffer set i mod n_sets and cohort range i mod n_ranges; those arguments
+    are built once, and each call goes straight to the ctypes function the
+    binding declares, so that a loop of small invocations spends no more host
+    time per launch than the C ABI itself (a one-cohort tiny invocation is
+    bound by that time)."""
+
+    def __init__(self, rc, h, sets, T, ranges, stream, bits=None):
+        import ctypes
+        import math
+        lib = rc.load_library()
+        self.rc, self.h, self.T = rc, h, T
+        self.chain_fn = lib.rc_cohort_run_chain
+        self.floor_fn = lib.rc_cohort_run_floor
+        self.stream = ctypes.c_void_p(stream)
+        self.bits = ctypes.c_void_p(bits.data_ptr()) if bits is not None else None
+        n_sets = len(sets.sets)
+        n = n_sets * len(ranges) // math.gcd(n_sets, len(ranges))
+        self.table = [(ctypes.byref(sets[i]),) + tuple(ranges[i % len(ranges)]) for i in range(n)]
+
+    def chain(self, n, mode, sync_each=False):
+        """n calls of rc_cohort_run_chain, table entries 0..n-1 (cyclic)."""
+        import torch
+        fn, h, T, st_h, tab = self.chain_fn, self.h, self.T, self.stream, self.table
+        m, base = len(tab), step_block(n)
+        sync = torch.cuda.current_stream().synchronize if sync_each else None
+        for i in range(n):
+            b, cb, ce = tab[i % m]
+            st = fn(h, b, ((base + i) * T) & 0xFFFFFFFF, T, mode, cb, ce, st_h)
+            if st:
+                raise self.rc.RcError(st, "rc_cohort_run_chain")
+            if sync:
+                sync()
+
+    def floor(self, n):
+        """n calls of rc_cohort_run_floor with the bitmap given at build."""
+        fn, h, T, st_h, tab, bits = self.floor_fn, self.h, self.T, self.stream, self.table, self.bits
+        m = len(tab)
+        for i in range(n):
+            b, cb, ce = tab[i % m]
+            st = fn(h, b, bits, T, cb, ce, st_h)
+            if st:
+                raise self.rc.RcError(st, "rc_cohort_run_floor")
+
+
+def time_resident(rc, h, sets, inp, T, steps, warmup, stream, ranges=None, calls=None):
     """Pipelined resident chains.  Returns the wall seconds of the timed loop
     and its GPU time (ms) from one HIP event pair around it, recorded on the
     stream the kernels are launched on (the current torch stream, whose
@@ -183,20 +235,15 @@ def time_resident(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
     launches, so region time / steps is the average launch duration plus the
     small gap between back-to-back launches."""
     import torch
-    C = inp.n_cohorts
-    rng = ranges or [(0, C)]
+    calls = calls or Launches(rc, h, sets, T, ranges or [(0, inp.n_cohorts)], stream)
     cur = torch.cuda.current_stream()
     assert cur.cuda_stream == stream
-    for i in range(warmup):
-        cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_RESIDENT, cb, ce, stream)
+    calls.chain(warmup, rc.RC_MODE_RESIDENT)
     r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     r0.record(cur)
-    for i in range(steps):
-        cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_RESIDENT, cb, ce, stream)
+    calls.chain(steps, rc.RC_MODE_RESIDENT)
     r1.record(cur)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -211,17 +258,20 @@ def time_resident(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
 CLOCK_WARMUP_S = 0.25
 
 
-def warm_clocks(launch, seconds=CLOCK_WARMUP_S):
-    """Untimed calls launch(i), in blocks of about 5 ms, until `seconds` of
-    wall time have passed.  Returns the calls made."""
+def warm_calls(calls, mode, seconds=CLOCK_WARMUP_S):
+    """Untimed calls (resident or host round trip by `mode`; the floor when
+    mode is None), in blocks of about 5 ms, until `seconds` of wall time
+    have passed.  Returns the calls made."""
     import torch
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     n, block = 0, 8
     while True:
         tb = time.perf_counter()
-        for i in range(block):
-            launch(n + i)
+        if mode is None:
+            calls.floor(block)
+        else:
+            calls.chain(block, mode)
         torch.cuda.synchronize()
         n += block
         now = time.perf_counter()
@@ -230,18 +280,12 @@ def warm_clocks(launch, seconds=CLOCK_WARMUP_S):
         block = int(max(1, min(4096, block * 0.005 / max(now - tb, 1e-6))))
 
 
-def resident_launcher(rc, h, sets, T, C, stream):
-    return lambda i: rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_RESIDENT, 0, C, stream)
-
-
-def time_resident_synced(rc, h, sets, inp, T, steps, stream, ranges):
+def time_resident_synced(rc, h, sets, inp, T, steps, stream, ranges, calls=None):
     import torch
+    calls = calls or Launches(rc, h, sets, T, ranges, stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(steps):
-        cb, ce = ranges[i % len(ranges)]
-        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_RESIDENT, cb, ce, stream)
-        torch.cuda.current_stream().synchronize()
+    calls.chain(steps, rc.RC_MODE_RESIDENT, sync_each=True)
     return time.perf_counter() - t0
 
 
@@ -278,36 +322,26 @@ def floor_bits(rc, h, inp, T, stream):
     return torch.from_numpy(bits.view(np.int32)).cuda()
 
 
-def time_floor(rc, h, sets, bits, inp, T, steps, warmup, stream, ranges=None):
+def time_floor(rc, h, sets, bits, inp, T, steps, warmup, stream, ranges=None, calls=None):
     """Pipelined no-decision-floor launches (same protocol as the resident
     chain).  Returns the wall seconds of the timed loop."""
     import torch
-    rng = ranges or [(0, inp.n_cohorts)]
-    ptr = bits.data_ptr()
-    for i in range(warmup):
-        cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_floor(h, sets[i], ptr, T, cb, ce, stream)
+    calls = calls or Launches(rc, h, sets, T, ranges or [(0, inp.n_cohorts)], stream, bits)
+    calls.floor(warmup)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(steps):
-        cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_floor(h, sets[i], ptr, T, cb, ce, stream)
+    calls.floor(steps)
     torch.cuda.synchronize()
     return time.perf_counter() - t0
 
 
-def time_hrt(rc, h, sets, inp, T, steps, warmup, stream, ranges=None):
+def time_hrt(rc, h, sets, inp, T, steps, warmup, stream, ranges=None, calls=None):
     import torch
-    C = inp.n_cohorts
-    rng = ranges or [(0, C)]
-    for i in range(warmup):
-        cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_HOST_ROUNDTRIP, cb, ce, stream)
+    calls = calls or Launches(rc, h, sets, T, ranges or [(0, inp.n_cohorts)], stream)
+    calls.chain(warmup, rc.RC_MODE_HOST_ROUNDTRIP)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(steps):
-        cb, ce = rng[i % len(rng)]
-        rc.rc_cohort_run_chain(h, sets[i], step0_next(T), T, rc.RC_MODE_HOST_ROUNDTRIP, cb, ce, stream)
+    calls.chain(steps, rc.RC_MODE_HOST_ROUNDTRIP)
     torch.cuda.synchronize()
     return time.perf_counter() - t0
 
@@ -384,11 +418,12 @@ def mechanism_row(rc, wk, key, rows=MECH_ROWS, row_s=MECH_ROW_S, common_count=Fa
         sets = Sets(rc, inp, T, n_sets)
         stream = torch.cuda.current_stream().cuda_stream
         bits = floor_bits(rc, h, inp, T, stream)
+        calls = Launches(rc, h, sets, T, ranges, stream, bits)
         timers = {
-            "resident": lambda k: time_resident(rc, h, sets, inp, T, k, 0, stream, ranges)[0],
-            "resident_synced": lambda k: time_resident_synced(rc, h, sets, inp, T, k, stream, ranges),
-            "floor": lambda k: time_floor(rc, h, sets, bits, inp, T, k, 0, stream, ranges),
-            "host_rt": lambda k: time_hrt(rc, h, sets, inp, T, k, 0, stream, ranges),
+            "resident": lambda k: time_resident(rc, h, sets, inp, T, k, 0, stream, ranges, calls)[0],
+            "resident_synced": lambda k: time_resident_synced(rc, h, sets, inp, T, k, stream, ranges, calls),
+            "floor": lambda k: time_floor(rc, h, sets, bits, inp, T, k, 0, stream, ranges, calls),
+            "host_rt": lambda k: time_hrt(rc, h, sets, inp, T, k, 0, stream, ranges, calls),
         }
         res = {}
         counts = {}
@@ -765,8 +800,9 @@ def measure_roofline(rc, wk, key, steps, warmup, warm=True):
         del probe
         sets = Sets(rc, inp, T, n_sets)
         stream = torch.cuda.current_stream().cuda_stream
-        n_warm = warm_clocks(resident_launcher(rc, h, sets, T, inp.n_cohorts, stream)) if warm else 0
-        _, region_ms = time_resident(rc, h, sets, inp, T, steps, warmup, stream)
+        calls = Launches(rc, h, sets, T, [(0, inp.n_cohorts)], stream)
+        n_warm = warm_calls(calls, rc.RC_MODE_RESIDENT) if warm else 0
+        _, region_ms = time_resident(rc, h, sets, inp, T, steps, warmup, stream, calls=calls)
         blk = roofline_of(key, inp, T, region_ms / steps)
         blk.update({"workload": wl.title, "launches_timed": steps, "buffer_sets_rotated": n_sets,
                     "clock_warmup_launches": n_warm})
@@ -972,8 +1008,9 @@ def main():
         verified = all(np.array_equal(t[k].cpu().numpy().view(np.uint32), want[k]) for k in want)
         sets = Sets(rc, inp, T, n_sets)  # fresh inputs again
 
-    n_warm = 0 if args.profile_only else warm_clocks(resident_launcher(rc, h, sets, T, C, stream))
-    wall, region_ms = time_resident(rc, h, sets, inp, T, args.steps, args.warmup, stream)
+    calls = Launches(rc, h, sets, T, [(0, C)], stream)
+    n_warm = 0 if args.profile_only else warm_calls(calls, rc.RC_MODE_RESIDENT)
+    wall, region_ms = time_resident(rc, h, sets, inp, T, args.steps, args.warmup, stream, calls=calls)
     trans_per_step = N * T
     value = trans_per_step * args.steps / wall
     ms_per_step = wall / args.steps * 1e3
@@ -1035,8 +1072,9 @@ def main():
             "launches_per_invocation": cnt[0], "d2h_copies_per_invocation": cnt[1], "steps": hs,
         }
         bits = floor_bits(rc, h, inp, T, stream)
-        warm_clocks(lambda i: rc.rc_cohort_run_floor(h, sets[i], bits.data_ptr(), T, 0, C, stream))
-        wall_f = time_floor(rc, h, sets, bits, inp, T, args.steps, args.warmup, stream)
+        fcalls = Launches(rc, h, sets, T, [(0, C)], stream, bits)
+        warm_calls(fcalls, None)
+        wall_f = time_floor(rc, h, sets, bits, inp, T, args.steps, args.warmup, stream, calls=fcalls)
         us_f = wall_f / args.steps * 1e6
         out["floor"] = {
             "us_per_invocation": round(us_f, 3), "us_per_chained_step": round(us_f / T, 4),
