@@ -87,3 +87,39 @@ def test_summarize_trace_counts_blocks(tmp_path, capsys):
     out = capsys.readouterr().out.strip().splitlines()
     assert out[2].startswith("| w | resident | 2 | 1.00 | 0.00 | 0.00 | 0.00 | (1, 0) |"), out[2]
     assert out[3].startswith("| w | host_rt | 2 | 9.00 | 3.00 | 3.00 | 3.00 | (9, 3) |"), out[3]
+
+
+class _FakeSets:
+    """Stand-in for bench.Sets: n buffer sets, no device memory."""
+
+    def __init__(self, rc, n):
+        self.sets = [(None, rc.RcBuffers(0x1000 * (i + 1), 0, 0, 0, 0, 0, 64)) for i in range(n)]
+
+    def __getitem__(self, i):
+        return self.sets[i % len(self.sets)][1]
+
+
+def test_launch_table_and_step_clock():
+    """The timing loops' pre-bound calls: invocation i uses buffer set
+    i mod n_sets and cohort range i mod n_ranges (the table repeats after
+    their least common multiple), and every call continues the step clock
+    (step0 = invocations so far times T), across calls of the loop."""
+    from paper_2608_12123_amd import rc_cohort as rc
+    sets = _FakeSets(rc, 4)
+    ranges = [(c, c + 1) for c in range(6)]
+    calls = bench.Launches(rc, "handle", sets, 8, ranges, 0)
+    assert len(calls.table) == 12
+    for i, (b, cb, ce) in enumerate(calls.table):
+        assert b._obj is sets[i % 4] and (cb, ce) == ranges[i % 6]
+    seen = []
+    calls.chain_fn = lambda h, b, step0, T, mode, cb, ce, st: seen.append((b._obj, step0, T, mode, cb, ce)) or 0
+    base = bench._STEP_CLOCK[0]
+    calls.chain(5, rc.RC_MODE_RESIDENT)
+    calls.chain(3, rc.RC_MODE_HOST_ROUNDTRIP)
+    assert [s[1] for s in seen] == [((base + i) * 8) & 0xFFFFFFFF for i in range(5)] + \
+        [((base + 5 + i) * 8) & 0xFFFFFFFF for i in range(3)]
+    assert [s[0] for s in seen[5:]] == [sets[0], sets[1], sets[2]]  # each loop starts at entry 0
+    assert [s[3] for s in seen] == [rc.RC_MODE_RESIDENT] * 5 + [rc.RC_MODE_HOST_ROUNDTRIP] * 3
+    calls.chain_fn = lambda *a: rc.RC_E_INVALID
+    with pytest.raises(rc.RcError):
+        calls.chain(1, rc.RC_MODE_RESIDENT)
