@@ -801,9 +801,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 // Rows of the mask image are W + 4 words apart (one zero block of padding
 // shifts consecutive rows across the LDS banks), so block q of a row is an
 // immediate offset from the row's byte offset.
-// PIPED (W = 32): the A lanes keep only the chain and run it one 4-step
-// chunk ahead; the B lanes replay every word and emit the effects (see PIPE
-// below).
+// PIPED (W = 32): three lanes per session; the A lanes keep only the chain
+// and run it one 4-step chunk ahead, the B lanes replay words [0, 8) and
+// emit the effects, the C lanes replay the rest (see PIPE below).
 // FLOOR: the no-decision floor -- the A lanes read every decision from the
 // bitmap instead of computing it (SPLIT: the first two chunks' words issued
 // with the staging loads, later chunks' a chunk ahead).
@@ -817,24 +817,30 @@ struct ChainF {
     // waiting for everything on the vector-memory counter, so a lane that
     // emits effects should have no load left to wait for -- and the 28 words
     // of the B lanes then arrive while the effects go out.
-    // PIPE (PIPED, SPLIT at WMAX = 32): the A lanes hold only word 0 and
-    // the outcome and run the chain one 4-step chunk ahead, storing nothing
-    // but the final outcome; the B lanes hold all the words, replay each
-    // chunk behind it and emit the effects.  The chain of chunk k + 1 then
-    // overlaps the replay of chunk k, where the two-role split runs its
-    // 16-step chunks' chains and replays in turn.  The B lanes carry more
-    // work per step, so this pays only for chains longer than one 16-step
-    // chunk in launches of at most one workgroup per CU (the host decides).
+    // PIPE (PIPED, SPLIT at WMAX = 32): three lanes per session.  The A
+    // lanes hold only word 0 and the outcome and run the chain one 4-step
+    // chunk ahead, storing nothing but the final outcome; behind it, the B
+    // lanes replay each chunk over words [0, WP1) and emit the effects, and
+    // the C lanes replay it over words [WP1, WMAX).  The chain of chunk
+    // k + 1 then overlaps the replay of chunk k, where the two-role split
+    // runs its 16-step chunks' chains and replays in turn; splitting the
+    // replay over two roles gives it eight wavefronts per cohort to hide its
+    // LDS and dependence latency.  The replay starts after one 4-step chunk,
+    // so its state loads are not hidden behind a 16-step chain: with more
+    // than one workgroup per CU and a one-operation route (mod R) the
+    // two-role split is faster (the host decides).
     static constexpr bool PIPE = SPLIT && WMAX == 32 && PIPED;
+    static constexpr int WP1 = 8;  // PIPE: words of the B lanes (the C lanes hold the rest)
+    static constexpr int NROLE = PIPE ? 3 : SPLIT ? 2 : 1;
     static constexpr int WA = PIPE ? 0 : SPLIT ? (WMAX == 32 ? 4 : WMAX / 2) : WMAX;
     static constexpr int WB = SPLIT ? WMAX - WA : 0;
-    static constexpr int WS = WA > WB ? WA : WB;  // state registers per lane
+    static constexpr int WS = PIPE ? WMAX - WP1 : (WA > WB ? WA : WB);  // state registers per lane
     static constexpr int NBA = WA / 4, NBB = WB / 4;  // 16-byte blocks per lane
     static constexpr uint32_t RS = (WMAX + 4) * 4;       // row stride in bytes
     // steps per chunk (PIPE: two chunks in flight, each in its own half of
     // the 16-step control and count areas)
     static constexpr int TC = PIPE ? 4 : WMAX <= 32 ? 16 : 8;
-    static constexpr uint32_t WG = (SPLIT ? 2 : 1) * NWAVE * 64;
+    static constexpr uint32_t WG = NROLE * NWAVE * 64;
     static constexpr int SB = WMAX <= 32 ? (SPLIT ? 5 : 10) : (SPLIT ? 3 : 6);
     static constexpr uint32_t NLA = NWAVE * 64;  // lanes of the plan's sessions (the A lanes)
     // Bins of sub-wavefront cohorts (each cohort inside one wavefront) pass
@@ -857,10 +863,12 @@ struct ChainF {
         const uint32_t tid = threadIdx.x;
         const uint32_t lane = tid & 63u;
         const uint32_t wv = uni(tid >> 6);
-        const bool role_b = SPLIT && wv >= (uint32_t)NWAVE;  // uniform per wavefront
-        const uint32_t wa = role_b ? wv - NWAVE : wv;         // the plan wavefront it serves
+        // 0: A; 1: B; 2 (PIPE): C -- uniform per wavefront
+        const uint32_t role = SPLIT ? uni(wv / (uint32_t)NWAVE) : 0u;
+        const bool role_b = role != 0u;
+        const uint32_t wa = wv - role * (uint32_t)NWAVE;      // the plan wavefront it serves
         const uint32_t alane = wa * 64u + lane;                // lane index among the A lanes
-        const uint32_t wbase = role_b ? (uint32_t)WA : 0u;    // first word of this lane
+        const uint32_t wbase = PIPE ? (role == 2u ? (uint32_t)WP1 : 0u) : (role_b ? (uint32_t)WA : 0u);  // first word
         const uint32_t W = a.n_words;
         const uint32_t R = a.ra.n_routes;
         const uint32_t T = a.n_steps;
@@ -960,7 +968,10 @@ struct ChainF {
         };
         auto stage_b = [&]() {
             const uint32_t c4 = a.chain_words / 4u;
-            for (uint32_t blk = wa; c4 + blk * 64u < n4; blk += NWAVE) {
+            // PIPE: the B and C wavefronts share the blocks
+            const uint32_t b0 = PIPE ? (role - 1u) * (uint32_t)NWAVE + wa : wa;
+            constexpr uint32_t BSTR = PIPE ? 2u * NWAVE : NWAVE;
+            for (uint32_t blk = b0; c4 + blk * 64u < n4; blk += BSTR) {
                 const uint32_t j = c4 + blk * 64u + lane;
                 if (j < n4)
                     __builtin_amdgcn_global_load_lds((const void*)(src + j), (lds_void*)(lds4 + c4 + blk * 64u),
@@ -1309,11 +1320,6 @@ struct ChainF {
             } else {
                 stage_b();
                 bare_barrier();
-                load_words(std::integral_constant<int, WB>{});
-                // the row loads issued before the WB state loads have landed
-                // (with W < WMAX fewer state loads were issued: wait for all)
-                wait_vmcnt<EXACT ? WB : 0>();
-                lds_barrier();
                 auto read_ctl = [&](uint32_t t0) {
                     const uint32_t par = half_of(t0);
 #pragma unroll
@@ -1322,15 +1328,30 @@ struct ChainF {
                         add[i] = lds_add[(par + i) * NLA + alane];
                     }
                 };
-                read_ctl(0u);
-                wait_vmcnt<0>();  // every word is needed at the first step
-                replay(0u, Z{}, NB{}, Yes{}, No{});
-                for (uint32_t t0 = TC; t0 < T; t0 += TC) {
+                // B (words [0, WP1), effects) and C (the rest): the same
+                // barriers, each with its own straight-line sequence
+                auto replay_role = [&](auto nw_c, auto nq_c, auto eff_c) {
+                    constexpr int NWR = decltype(nw_c)::value;
+                    load_words(nw_c);
+                    // the row loads issued before the NWR state loads have
+                    // landed (with W < WMAX fewer were issued: wait for all)
+                    wait_vmcnt<EXACT ? NWR : 0>();
                     lds_barrier();
-                    read_ctl(t0);
-                    replay(t0, Z{}, NB{}, Yes{}, No{});
-                }
-                store_state(std::integral_constant<int, WB>{}, false);
+                    read_ctl(0u);
+                    wait_vmcnt<0>();  // every word is needed at the first step
+                    replay(0u, Z{}, nq_c, eff_c, No{});
+                    for (uint32_t t0 = TC; t0 < T; t0 += TC) {
+                        lds_barrier();
+                        read_ctl(t0);
+                        replay(t0, Z{}, nq_c, eff_c, No{});
+                    }
+                    store_state(nw_c, false);
+                };
+                if (role == 1u)
+                    replay_role(std::integral_constant<int, WP1>{}, std::integral_constant<int, WP1 / 4>{}, Yes{});
+                else
+                    replay_role(std::integral_constant<int, WMAX - WP1>{},
+                                std::integral_constant<int, (WMAX - WP1) / 4>{}, No{});
             }
         } else if constexpr (SPLIT) {
             if (!role_b) {
@@ -1401,12 +1422,15 @@ struct ChainF {
 };
 
 // One workgroup per bin: blocks [0, bins_a_n) take the sub-wavefront bins,
-// the rest the multi-wavefront bins.  The table-image chain and the two-lane
+// the rest the multi-wavefront bins.  The table-image chain and the two-role
 // full-image chain at W <= 32 run two 512-lane workgroups per CU, so they are
-// held to four wavefronts per SIMD (at most 128 VGPRs).  At W = 64 the
-// two-lane full-image chain needs more registers and runs one per CU.
+// held to four wavefronts per SIMD (at most 128 VGPRs); the pipelined split
+// runs two 768-lane workgroups per CU, six wavefronts per SIMD (at most 80
+// VGPRs).  At W = 64 the two-lane full-image chain needs more registers and
+// runs one per CU.
 template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool FLOOR, bool PIPED>
-__global__ __launch_bounds__((FULL && WMAX >= 32 ? 2 : 1) * NWAVE * 64, (!FULL || WMAX == 32) ? 4 : 1)
+__global__ __launch_bounds__((FULL && WMAX >= 32 ? (PIPED && WMAX == 32 ? 3 : 2) : 1) * NWAVE * 64,
+                             (!FULL || WMAX == 32) ? (PIPED && FULL && WMAX == 32 ? 6 : 4) : 1)
 void rc_chain_kernel(ChainArgs a) {
     extern __shared__ uint4 lds4[];
     if constexpr (FULL) {
@@ -1595,12 +1619,16 @@ ChainFn pick_chain(uint32_t wmax, bool exact, bool full, bool piped, int rk, boo
                  : pick_chain_t<false>(wmax, exact, full, piped, rk);
 }
 
-// The pipelined split for a launch: chains longer than one 16-step chunk,
-// at most one workgroup per CU.  Measured on MI355X (256-session cohorts,
-// W = 32): 6-10% faster than the two-role split from 1 to 256 workgroups at
-// T = 32, slower beyond that and at every size for T <= 16.
-bool use_piped(uint32_t wmax, bool full, uint32_t T, uint32_t grid, uint32_t n_cu) {
-    return has_piped(wmax, full) && T > 16u && grid <= n_cu;
+// The pipelined split for a launch: at most one workgroup per CU, or a
+// chain whose route is a threshold search (CDF mode), whose longer step
+// makes the overlap pay at any launch size.  Measured on MI355X
+// (256-session cohorts, W = 32, every launch streaming from HBM): 4-15%
+// faster than the two-role split from 1 to 256 workgroups with mod-R
+// routes, 5-27% faster at every size with CDF routes; with mod-R routes
+// beyond one workgroup per CU it ties or loses (the 100,000-session chain:
+// 16.3-16.6 against 14.8-15.4 us).
+bool use_piped(uint32_t wmax, bool full, int route_kind, uint32_t grid, uint32_t n_cu) {
+    return has_piped(wmax, full) && (grid <= n_cu || route_kind == RK_CDF);
 }
 
 template <int WMAX, bool EXACT>
@@ -1848,9 +1876,11 @@ int run_resident(rc_cohort* h, const rc_buffers* b, uint32_t step0, uint32_t T,
     a.dbits = dbits;
     a.dwords = (b->ld + 31u) / 32u;
     const uint32_t grid = a.bins_a_n + a.bins_b_n;  // one workgroup per bin
-    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, use_piped(h->wmax, h->full, T, grid, h->n_cu),
-                            h->route_kind, dbits != nullptr);
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(h->chain_threads), h->chain_lds_bytes, stream, a);
+    const bool piped = use_piped(h->wmax, h->full, h->route_kind, grid, h->n_cu);
+    ChainFn fn = pick_chain(h->wmax, h->exact, h->full, piped, h->route_kind, dbits != nullptr);
+    // the pipelined split runs three lanes per session, the two-role split two
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(piped ? 3u * 64u * h->nwave : h->chain_threads), h->chain_lds_bytes,
+                       stream, a);
     if (launch_ok() != RC_OK) return RC_E_DEVICE;
     h->last_launches = 1;
     h->last_d2h = 0;

@@ -148,18 +148,21 @@ def test_floor_invalid_arguments_touch_nothing():
         co.close()
 
 
-def test_floor_both_two_lane_kernels(orc):
-    """W = 32, T = 32 with the oracle's recorded decisions: one launch of
-    1,000 cohorts (the two-role split, two 16-step chunks) and launches of at
-    most 256 cohorts (the pipelined split, 4-step chunks) reproduce the
-    oracle's chain."""
-    wl = wk.WORKLOADS["k256"]
-    inp = wk.make_inputs(wl, chunk=2)
-    C, T = inp.n_cohorts, wl.n_steps
+def test_floor_both_w32_kernels(orc):
+    """W = 32, T = 32, mod-R routes, with the oracle's recorded decisions: one
+    launch of 600 cohorts (more workgroups than CUs: the two-role split) and
+    launches of at most 256 cohorts (the pipelined three-role split)
+    reproduce the oracle's chain."""
+    T = 32
+    rng = np.random.Generator(np.random.PCG64(72_000))
+    sizes = [int(x) for x in rng.choice([256, 256, 256, 200, 129, 128, 64, 40, 32, 1], size=600)]
+    inp = wk.make_custom(n_words=32, n_routes=256, route_mode=wk.ROUTE_MOD, decide_thr=32768,
+                         cohort_sizes=sizes, n_steps=T, seed_key=72_000, ld=sum(sizes) + 3)
+    C = inp.n_cohorts
     say("floor, both two-lane kernels: C=%d T=%d" % (C, T))
     want = orc.run_inputs(inp, n_steps=T, record=True)
     whole = gpu_floor(inp, want["decisions"], T, [(0, C)])
     assert_same(whole, want, "one launch")
-    cuts = [0, 256, 257, 513, 769, C]
+    cuts = [0, 256, 257, 400, C]
     pieces = gpu_floor(inp, want["decisions"], T, list(zip(cuts[:-1], cuts[1:])))
     assert_same(pieces, want, "launches of at most 256 cohorts")

@@ -257,11 +257,44 @@ def test_empty_calls_are_noops():
         co.close()
 
 
+def w32_mod_inputs(T, seed_key):
+    """W = 32 with mod-R routes (R = 256) in 600 cohorts, sub-wavefront and
+    multi-wavefront sizes mixed, so that a launch of all of them takes more
+    workgroups than the device has CUs."""
+    rng = np.random.Generator(np.random.PCG64(seed_key))
+    sizes = [int(x) for x in rng.choice([256, 256, 256, 200, 129, 128, 64, 40, 32, 1], size=600)]
+    return wk.make_custom(n_words=32, n_routes=256, route_mode=wk.ROUTE_MOD, decide_thr=32768,
+                          cohort_sizes=sizes, n_steps=T, seed_key=seed_key, ld=sum(sizes) + 3)
+
+
+@pytest.mark.parametrize("T", [16, 32])
 @pytest.mark.parametrize("mode", sorted(MODES))
-def test_both_two_lane_kernels(orc, mode):
-    """W = 32, T = 32: one launch of 1,000 cohorts (more workgroups than CUs:
-    the two-role split, two 16-step chunks) and the same cohorts in launches
-    of 1, 100 and 256 (the pipelined split, eight 4-step chunks)."""
+def test_both_w32_kernels(orc, mode, T):
+    """W = 32, mod-R routes: one launch of every cohort (more workgroups than
+    CUs: the two-role split, 16-step chunks) and the same cohorts in launches
+    of 1 to 256 cohorts (the pipelined three-role split, 4-step chunks)."""
+    inp = w32_mod_inputs(T, 71_000 + T)
+    C = inp.n_cohorts
+    co = rc.Cohort.from_inputs(inp, max_steps=T)
+    try:
+        grid = co.plan_info()[0]
+    finally:
+        co.close()
+    say("both W=32 kernels mode=%s C=%d workgroups=%d T=%d" % (mode, C, grid, T))
+    assert grid > 256
+    want = oracle_run(orc, inp, T, step0=11)
+    whole = gpu_run_ranges(inp, T, MODES[mode], [(0, C)], step0=11)
+    assert_same(whole, want, "one launch")
+    cuts = [0, 1, 101, 300, 520, C]
+    pieces = gpu_run_ranges(inp, T, MODES[mode], list(zip(cuts[:-1], cuts[1:])), step0=11)
+    assert_same(pieces, want, "launches of 1 to 220 cohorts")
+
+
+@pytest.mark.parametrize("mode", sorted(MODES))
+def test_cdf_routes_pipelined_at_every_size(orc, mode):
+    """W = 32, T = 32, CDF routes (the k256 shape): the pipelined split at
+    every launch size -- one launch of 1,000 cohorts, and launches of 1, 100
+    and 256."""
     wl = wk.WORKLOADS["k256"]
     inp = wk.make_inputs(wl, chunk=1)
     C, T = inp.n_cohorts, wl.n_steps

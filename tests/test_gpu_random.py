@@ -84,8 +84,9 @@ def test_random_shape(orc, case):
 
 
 def draw_two_lane(case):
-    """Shapes of the pipelined two-lane kernel: W 17..32, a route count whose
-    full mask image fits, T > 16, launches of at most 256 cohorts."""
+    """Shapes of the pipelined three-role kernel: W 17..32, a route count
+    whose full mask image fits, long chains (T > 16), launches of at most
+    256 cohorts."""
     rng = np.random.Generator(np.random.PCG64(92_000 + case))
     W = int(rng.integers(17, 33))
     R = int(rng.choice([1, 3, 16, 64, 200, 256, 400]))
