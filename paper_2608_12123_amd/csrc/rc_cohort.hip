@@ -801,9 +801,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 // Rows of the mask image are W + 4 words apart (one zero block of padding
 // shifts consecutive rows across the LDS banks), so block q of a row is an
 // immediate offset from the row's byte offset.
-// PIPED (W = 32): three lanes per session; the A lanes keep only the chain
-// and run it one 4-step chunk ahead, the B lanes replay words [0, 8) and
-// emit the effects, the C lanes replay the rest (see PIPE below).
+// PIPED (W <= 32, WMAX = 16 or 32): three lanes per session; the A lanes
+// keep only the chain and run it one 4-step chunk ahead, the B lanes replay
+// words [0, 8) and emit the effects, the C lanes replay the rest (see PIPE
+// below).
 // FLOOR: the no-decision floor -- the A lanes read every decision from the
 // bitmap instead of computing it (SPLIT: the first two chunks' words issued
 // with the staging loads, later chunks' a chunk ahead).
@@ -817,7 +818,7 @@ struct ChainF {
     // waiting for everything on the vector-memory counter, so a lane that
     // emits effects should have no load left to wait for -- and the 28 words
     // of the B lanes then arrive while the effects go out.
-    // PIPE (PIPED, SPLIT at WMAX = 32): three lanes per session.  The A
+    // PIPE (PIPED at WMAX = 16 or 32): three lanes per session.  The A
     // lanes hold only word 0 and the outcome and run the chain one 4-step
     // chunk ahead, storing nothing but the final outcome; behind it, the B
     // lanes replay each chunk over words [0, WP1) and emit the effects, and
@@ -829,7 +830,7 @@ struct ChainF {
     // so its state loads are not hidden behind a 16-step chain: with more
     // than one workgroup per CU and a one-operation route (mod R) the
     // two-role split is faster (the host decides).
-    static constexpr bool PIPE = SPLIT && WMAX == 32 && PIPED;
+    static constexpr bool PIPE = SPLIT && (WMAX == 32 || WMAX == 16) && PIPED;
     static constexpr int WP1 = 8;  // PIPE: words of the B lanes (the C lanes hold the rest)
     static constexpr int NROLE = PIPE ? 3 : SPLIT ? 2 : 1;
     static constexpr int WA = PIPE ? 0 : SPLIT ? (WMAX == 32 ? 4 : WMAX / 2) : WMAX;
@@ -1425,16 +1426,18 @@ struct ChainF {
 // the rest the multi-wavefront bins.  The table-image chain and the two-role
 // full-image chain at W <= 32 run two 512-lane workgroups per CU, so they are
 // held to four wavefronts per SIMD (at most 128 VGPRs); the pipelined split
-// runs two 768-lane workgroups per CU, six wavefronts per SIMD (at most 80
-// VGPRs).  At W = 64 the two-lane full-image chain needs more registers and
+// (W <= 32) runs two 768-lane workgroups per CU, six wavefronts per SIMD
+// (at most 80 VGPRs).  At W = 64 the two-lane full-image chain needs more registers and
 // runs one per CU.
 template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool FLOOR, bool PIPED>
-__global__ __launch_bounds__((FULL && WMAX >= 32 ? (PIPED && WMAX == 32 ? 3 : 2) : 1) * NWAVE * 64,
-                             (!FULL || WMAX == 32) ? (PIPED && FULL && WMAX == 32 ? 6 : 4) : 1)
+__global__ __launch_bounds__((FULL && (WMAX >= 32 || (PIPED && WMAX == 16)) ? (PIPED && WMAX <= 32 ? 3 : 2) : 1) *
+                                 NWAVE * 64,
+                             (!FULL || WMAX == 32) ? (PIPED && FULL && WMAX == 32 ? 6 : 4)
+                                                   : (PIPED && WMAX == 16 ? 6 : 1))
 void rc_chain_kernel(ChainArgs a) {
     extern __shared__ uint4 lds4[];
     if constexpr (FULL) {
-        constexpr bool SPLIT = WMAX >= 32;
+        constexpr bool SPLIT = WMAX >= 32 || (PIPED && WMAX == 16);
         if (blockIdx.x < a.bins_a_n)
             ChainF<WMAX, EXACT, NWAVE, RK, false, SPLIT, FLOOR, PIPED>::run(a, a.bins_a_lo + blockIdx.x, lds4);
         else
@@ -1582,8 +1585,8 @@ typedef void (*ChainFn)(ChainArgs);
 typedef void (*DecideFn)(DecideArgs);
 typedef void (*BodyFn)(BodyArgs);
 
-// The pipelined split exists for the full image at WMAX = 32 only.
-bool has_piped(uint32_t wmax, bool full) { return full && wmax == 32u; }
+// The pipelined split exists for the full image at WMAX = 16 and 32.
+bool has_piped(uint32_t wmax, bool full) { return full && (wmax == 32u || wmax == 16u); }
 
 template <int WMAX, bool EXACT, int RK, bool FLOOR>
 ChainFn chain_fn(bool full, bool piped) {
@@ -1591,7 +1594,7 @@ ChainFn chain_fn(bool full, bool piped) {
         if constexpr (WMAX >= 32) return rc_chain_kernel<WMAX, EXACT, 8, false, RK, FLOOR, false>;
         return nullptr;
     }
-    if constexpr (WMAX == 32)
+    if constexpr (WMAX == 32 || WMAX == 16)
         if (piped) return rc_chain_kernel<WMAX, EXACT, 4, true, RK, FLOOR, true>;
     return rc_chain_kernel<WMAX, EXACT, 4, true, RK, FLOOR, false>;
 }
@@ -1626,7 +1629,9 @@ ChainFn pick_chain(uint32_t wmax, bool exact, bool full, bool piped, int rk, boo
 // faster than the two-role split from 1 to 256 workgroups with mod-R
 // routes, 5-27% faster at every size with CDF routes; with mod-R routes
 // beyond one workgroup per CU it ties or loses (the 100,000-session chain:
-// 16.3-16.6 against 14.8-15.4 us).
+// 16.3-16.6 against 14.8-15.4 us).  At W = 16 against the one-lane chain
+// (64-session cohorts, T = 8, mod-16 routes): one cohort 6.42 -> 4.82 us,
+// 1,000 cohorts in 250 workgroups 8.55 -> 6.5 us.
 bool use_piped(uint32_t wmax, bool full, int route_kind, uint32_t grid, uint32_t n_cu) {
     return has_piped(wmax, full) && (grid <= n_cu || route_kind == RK_CDF);
 }
@@ -2082,14 +2087,17 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     const size_t lds_image = (size_t)h->img_words * 4u;
     h->nwave = h->full ? 4u : 8u;
     // image, then the count exchange ([16][nwave + 4] words; the table chain
-    // uses the first [2][nwave + 4]), then (full image, W >= 32: two lanes
-    // per session) the control handed to the second lanes, 16 steps of a
-    // 4-byte addend and a 2-byte control word per lane, then (full image)
-    // the effect stage of sub-wavefront bins, 4 + 16 bytes per lane
+    // uses the first [2][nwave + 4]), then (full image, WMAX >= 16: the
+    // two-role or the pipelined split) the control handed to the replaying
+    // lanes, 16 steps of a 4-byte addend and a 2-byte control word per lane,
+    // then (full image) the effect stage of sub-wavefront bins, 4 + 16 bytes
+    // per lane.  chain_threads is the two-role (W >= 32) or one-lane
+    // workgroup; the pipelined split launches three lanes per session.
     const bool split = h->full && h->wmax >= 32u;
+    const bool ctl_area = h->full && h->wmax >= 16u;
     const uint32_t na = h->nwave * 64u;
     h->chain_threads = (split ? 2u : 1u) * na;
-    h->chain_lds_bytes = lds_image + 16u * (h->nwave + 4u) * 4u + (split ? 16u * na * 6u : 0u) +
+    h->chain_lds_bytes = lds_image + 16u * (h->nwave + 4u) * 4u + (ctl_area ? 16u * na * 6u : 0u) +
                          (h->full ? na * 20u : 0u);
 
     h->offsets.assign(desc->cohort_offsets, desc->cohort_offsets + h->C + 1u);

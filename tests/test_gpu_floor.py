@@ -148,18 +148,19 @@ def test_floor_invalid_arguments_touch_nothing():
         co.close()
 
 
-def test_floor_both_w32_kernels(orc):
-    """W = 32, T = 32, mod-R routes, with the oracle's recorded decisions: one
-    launch of 600 cohorts (more workgroups than CUs: the two-role split) and
-    launches of at most 256 cohorts (the pipelined three-role split)
-    reproduce the oracle's chain."""
+@pytest.mark.parametrize("W", [32, 16])
+def test_floor_both_full_image_kernels(orc, W):
+    """T = 32, mod-R routes, with the oracle's recorded decisions: one launch
+    of 600 cohorts (more workgroups than CUs: the two-role split at W = 32,
+    the one-lane chain at W = 16) and launches of at most 256 cohorts (the
+    pipelined three-role split) reproduce the oracle's chain."""
     T = 32
-    rng = np.random.Generator(np.random.PCG64(72_000))
+    rng = np.random.Generator(np.random.PCG64(72_000 + W))
     sizes = [int(x) for x in rng.choice([256, 256, 256, 200, 129, 128, 64, 40, 32, 1], size=600)]
-    inp = wk.make_custom(n_words=32, n_routes=256, route_mode=wk.ROUTE_MOD, decide_thr=32768,
-                         cohort_sizes=sizes, n_steps=T, seed_key=72_000, ld=sum(sizes) + 3)
+    inp = wk.make_custom(n_words=W, n_routes=256, route_mode=wk.ROUTE_MOD, decide_thr=32768,
+                         cohort_sizes=sizes, n_steps=T, seed_key=72_000 + W, ld=sum(sizes) + 3)
     C = inp.n_cohorts
-    say("floor, both two-lane kernels: C=%d T=%d" % (C, T))
+    say("floor, both full-image kernels: W=%d C=%d T=%d" % (W, C, T))
     want = orc.run_inputs(inp, n_steps=T, record=True)
     whole = gpu_floor(inp, want["decisions"], T, [(0, C)])
     assert_same(whole, want, "one launch")

@@ -257,30 +257,31 @@ def test_empty_calls_are_noops():
         co.close()
 
 
-def w32_mod_inputs(T, seed_key):
-    """W = 32 with mod-R routes (R = 256) in 600 cohorts, sub-wavefront and
+def mod_route_inputs(W, T, seed_key):
+    """W words with mod-R routes (R = 256) in 600 cohorts, sub-wavefront and
     multi-wavefront sizes mixed, so that a launch of all of them takes more
     workgroups than the device has CUs."""
     rng = np.random.Generator(np.random.PCG64(seed_key))
     sizes = [int(x) for x in rng.choice([256, 256, 256, 200, 129, 128, 64, 40, 32, 1], size=600)]
-    return wk.make_custom(n_words=32, n_routes=256, route_mode=wk.ROUTE_MOD, decide_thr=32768,
+    return wk.make_custom(n_words=W, n_routes=256, route_mode=wk.ROUTE_MOD, decide_thr=32768,
                           cohort_sizes=sizes, n_steps=T, seed_key=seed_key, ld=sum(sizes) + 3)
 
 
-@pytest.mark.parametrize("T", [16, 32])
+@pytest.mark.parametrize("W,T", [(32, 16), (32, 32), (16, 8), (13, 20)])
 @pytest.mark.parametrize("mode", sorted(MODES))
-def test_both_w32_kernels(orc, mode, T):
-    """W = 32, mod-R routes: one launch of every cohort (more workgroups than
-    CUs: the two-role split, 16-step chunks) and the same cohorts in launches
-    of 1 to 256 cohorts (the pipelined three-role split, 4-step chunks)."""
-    inp = w32_mod_inputs(T, 71_000 + T)
+def test_both_full_image_kernels(orc, mode, W, T):
+    """Mod-R routes: one launch of every cohort (more workgroups than CUs:
+    the two-role split at W = 32, the one-lane chain at W <= 16) and the same
+    cohorts in launches of 1 to 220 cohorts (the pipelined three-role split,
+    4-step chunks)."""
+    inp = mod_route_inputs(W, T, 71_000 + 64 * W + T)
     C = inp.n_cohorts
     co = rc.Cohort.from_inputs(inp, max_steps=T)
     try:
         grid = co.plan_info()[0]
     finally:
         co.close()
-    say("both W=32 kernels mode=%s C=%d workgroups=%d T=%d" % (mode, C, grid, T))
+    say("both full-image kernels mode=%s W=%d C=%d workgroups=%d T=%d" % (mode, W, C, grid, T))
     assert grid > 256
     want = oracle_run(orc, inp, T, step0=11)
     whole = gpu_run_ranges(inp, T, MODES[mode], [(0, C)], step0=11)
