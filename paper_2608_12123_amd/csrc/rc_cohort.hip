@@ -874,19 +874,19 @@ struct ChainF {
         const uint32_t R = a.ra.n_routes;
         const uint32_t T = a.n_steps;
         // The host reserves 16 steps of each: counts [16][NWAVE + 4], then
-        // (SPLIT) the control handed to the B lanes -- addends [16][NLA] and
-        // 16-bit control words [16][NLA] -- then the effect stage of
-        // sub-wavefront bins.  PIPE uses the first 2 TC steps of the count and control
-        // areas (two chunks in flight).
+        // (SPLIT) the control handed to the replaying lanes -- addends
+        // [16][NLA] and control words [16][NLA] -- then the effect stage of
+        // sub-wavefront bins.  PIPE uses the first 2 TC steps of the count and
+        // control areas (two chunks in flight).
         static_assert(TC <= 16 && (!PIPE || 2 * TC <= 16), "LDS control and count areas hold 16 steps");
         uint32_t* lds_cnt = lds + a.img_words;
         uint32_t* lds_add = lds_cnt + 16 * CNT_STRIDE;
-        uint16_t* lds_ctl = reinterpret_cast<uint16_t*>(lds_add + (SPLIT ? 16 * NLA : 0));
+        uint32_t* lds_ctl = lds_add + (SPLIT ? 16 * NLA : 0);
         uint32_t* stage_w = reinterpret_cast<uint32_t*>(lds_ctl + (SPLIT ? 16 * NLA : 0));
         uint4* stage_p = reinterpret_cast<uint4*>(stage_w + NLA);
         const uint32_t* lds_tools = lds + a.tools_off;
 
-        const uint32_t* lds_rows = lds + a.rows_off;
+        const uint32_t rows_b = a.rows_off * 4u;  // byte offset of the mask rows in LDS
         const LaneCohort L = lane_cohort(a.wdesc + ((size_t)bin * NWAVE + wa) * WD_WORDS,
                                          a.offsets, lane, a.cohort_begin, a.cohort_end);
         const uint32_t soff = L.s << 2;
@@ -1083,7 +1083,15 @@ struct ChainF {
                     const uint32_t sh = (31u - r) & 31u;
                     const uint32_t rot = sh & ~dmsk;  // rotation 0 when taken
                     const uint32_t oo = o & ~dmsk;
-                    ctl[i] = rot | (dmsk & 32u) | (r << 6);
+                    // the step's control word: the rotation (bits 0..4, also
+                    // the shift operand of the rotate), the decision (bit 5),
+                    // the route (bits 6..15, for the tool pair) and the LDS
+                    // address of the mask row the update reads -- route r's
+                    // when taken, the zero row R's when not -- in 16-byte units
+                    // (bits 16..31), made here in the latency-bound chain so
+                    // that every replaying lane reads its row with one shift
+                    ctl[i] = rot | (dmsk & 32u) | (r << 6) |
+                             (((rows_b + __umul24(dbit ? r : R, RS)) >> 4) << 16);
                     add[i] = oo;
                     s0 = (rotr32(s0, rot) ^ (m0 & dmsk)) + oo;
                     o = dev_fmix32(s0);
@@ -1112,7 +1120,7 @@ struct ChainF {
                 if constexpr (SPLIT) {
 #pragma unroll
                     for (int i = 0; i < TC; ++i) {
-                        lds_ctl[(par + i) * NLA + alane] = (uint16_t)ctl[i];  // ctl < 2^16
+                        lds_ctl[(par + i) * NLA + alane] = ctl[i];
                         lds_add[(par + i) * NLA + alane] = add[i];
                     }
                 }
@@ -1147,13 +1155,13 @@ struct ChainF {
             uint32_t cc[4] = {0u, 0u, 0u, 0u}, tpc = 0u;
             if constexpr (PREF) {
                 const uint32_t c = ctl[0];
-                const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
+                const uint32_t rowoff = ((c >> 16) << 4) + qoff;
 #pragma unroll
-                for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds_rows, rowoff + 16u * q);
+                for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds, rowoff + 16u * q);
                 if constexpr (EFF) {
 #pragma unroll
                     for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[k] : 0u;
-                    tpc = lds_tools[c >> 6];
+                    tpc = lds_tools[(c >> 6) & 0x3FFu];
                 }
             }
 #pragma unroll
@@ -1162,24 +1170,24 @@ struct ChainF {
                 uint32_t cn[4] = {0u, 0u, 0u, 0u}, tpn = 0u;
                 if constexpr (!PREF) {
                     const uint32_t c = ctl[i];
-                    const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
+                    const uint32_t rowoff = ((c >> 16) << 4) + qoff;
 #pragma unroll
-                    for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds_rows, rowoff + 16u * q);
+                    for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds, rowoff + 16u * q);
                     if constexpr (EFF) {
 #pragma unroll
                         for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[i * CNT_STRIDE + k] : 0u;
-                        tpc = lds_tools[c >> 6];
+                        tpc = lds_tools[(c >> 6) & 0x3FFu];
                     }
                 }
                 if (PREF && i + 1 < TC) {
                     const uint32_t c = ctl[i + 1];
-                    const uint32_t rowoff = __umul24((c >> 5) & 1u ? (c >> 6) : R, RS) + qoff;
+                    const uint32_t rowoff = ((c >> 16) << 4) + qoff;
 #pragma unroll
-                    for (int q = 0; q < NQ; ++q) mn[q] = lds128(lds_rows, rowoff + 16u * q);
+                    for (int q = 0; q < NQ; ++q) mn[q] = lds128(lds, rowoff + 16u * q);
                     if constexpr (EFF) {
 #pragma unroll
                         for (int k = 0; k < 4; ++k) cn[k] = MULTI ? cq0[(i + 1) * CNT_STRIDE + k] : 0u;
-                        tpn = lds_tools[c >> 6];
+                        tpn = lds_tools[(c >> 6) & 0x3FFu];
                     }
                 }
                 if ((uint32_t)i < nr) {
@@ -2089,7 +2097,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     // image, then the count exchange ([16][nwave + 4] words; the table chain
     // uses the first [2][nwave + 4]), then (full image, WMAX >= 16: the
     // two-role or the pipelined split) the control handed to the replaying
-    // lanes, 16 steps of a 4-byte addend and a 2-byte control word per lane,
+    // lanes, 16 steps of a 4-byte addend and a 4-byte control word per lane,
     // then (full image) the effect stage of sub-wavefront bins, 4 + 16 bytes
     // per lane.  chain_threads is the two-role (W >= 32) or one-lane
     // workgroup; the pipelined split launches three lanes per session.
@@ -2097,7 +2105,7 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     const bool ctl_area = h->full && h->wmax >= 16u;
     const uint32_t na = h->nwave * 64u;
     h->chain_threads = (split ? 2u : 1u) * na;
-    h->chain_lds_bytes = lds_image + 16u * (h->nwave + 4u) * 4u + (ctl_area ? 16u * na * 6u : 0u) +
+    h->chain_lds_bytes = lds_image + 16u * (h->nwave + 4u) * 4u + (ctl_area ? 16u * na * 8u : 0u) +
                          (h->full ? na * 20u : 0u);
 
     h->offsets.assign(desc->cohort_offsets, desc->cohort_offsets + h->C + 1u);
