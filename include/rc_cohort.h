@@ -193,7 +193,9 @@ int rc_cohort_run_chain(rc_cohort *h, const rc_buffers *b, uint32_t step0,
  * One kernel launch, enqueued on `hip_stream`; returns without waiting.
  * n_steps == 0 or an empty cohort range is a no-op.  Errors: those of
  * rc_cohort_run_chain, and RC_E_INVALID when `decisions` is NULL, overlaps a
- * buffer or is not device memory large enough for its extent.
+ * buffer, or does not lie with its whole extent inside one HIP allocation of
+ * the handle's device (the same check as the six buffers': sizing it is the
+ * caller's part).
  */
 int rc_cohort_run_floor(rc_cohort *h, const rc_buffers *b, const uint32_t *decisions,
                         uint32_t n_steps, uint32_t cohort_begin, uint32_t cohort_end,
