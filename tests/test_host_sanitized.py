@@ -44,7 +44,9 @@ def sanitized_lib(tmp_path_factory):
 def test_host_code_under_asan_and_ubsan(sanitized_lib):
     env = dict(os.environ)
     env["RC_COHORT_LIB"] = sanitized_lib
-    env["LD_PRELOAD"] = _runtime("libasan.so")
+    # the ASan runtime first, anything already preloaded kept after it
+    prev = env.get("LD_PRELOAD", "")
+    env["LD_PRELOAD"] = _runtime("libasan.so") + (":" + prev if prev else "")
     env["ASAN_OPTIONS"] = "detect_leaks=0:abort_on_error=1:verify_asan_link_order=0"
     env["UBSAN_OPTIONS"] = "halt_on_error=1:print_stacktrace=1"
     cmd = [sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider", "-m", "not gpu"] + TESTS
