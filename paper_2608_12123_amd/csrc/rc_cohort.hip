@@ -1135,8 +1135,8 @@ struct ChainF {
         // Replay of the chunk starting at t0 over this lane's 16-byte word
         // blocks [QLO, QHI), with (EFF: the A lanes, or the B lanes under
         // PIPE) the slots and effects, step by step.  PREF: the LDS reads of
-        // step i + 1 (mask blocks and, with EFF, counts and tool pair) are
-        // issued before step i is computed; past the chunk's last step they
+        // step i + 1 (mask blocks and, with EFF, the tool pair) are issued
+        // before step i is computed; past the chunk's last step they
         // read the zero row (valid addresses, values unused).  The step count
         // is re-read so that no per-step condition stays live across the
         // phases.
@@ -1151,44 +1151,45 @@ struct ChainF {
             const uint32_t nr = opaque_s(n);
             const uint32_t* cq0 = lds_cnt + (L.flags >> 24) + half_of(t0) * CNT_STRIDE;
             const uint32_t qoff = (wbase + 4u * QLO) * 4u;  // byte offset of the first block in a row
+            // Cohorts spanning wavefronts: the chunk's counts are all in LDS
+            // before its replay starts, so each wavefront combines them once
+            // per chunk, lane-parallel -- lane i holds step i's taken count
+            // of the cohort (n1v) and of its wavefronts before this one
+            // (prev) -- and each step takes its two values with a readlane
+            // (lanes past the chunk read valid count slots, unused).
+            uint32_t n1v = 0u, prev = 0u;
+            if constexpr (EFF && MULTI) {
+                const uint32_t* q = cq0 + (lane < (uint32_t)TC ? lane : 0u) * CNT_STRIDE;
+                const uint32_t c0 = q[0], c1 = q[1], c2 = q[2], c3 = q[3];
+                n1v = (g[0] ? c0 : 0u) + (g[1] ? c1 : 0u) + (g[2] ? c2 : 0u) + (g[3] ? c3 : 0u);
+                prev = (f[0] ? c0 : 0u) + (f[1] ? c1 : 0u) + (f[2] ? c2 : 0u);
+            }
             uint4 mc[NQ];
-            uint32_t cc[4] = {0u, 0u, 0u, 0u}, tpc = 0u;
+            uint32_t tpc = 0u;
             if constexpr (PREF) {
                 const uint32_t c = ctl[0];
                 const uint32_t rowoff = ((c >> 16) << 4) + qoff;
 #pragma unroll
                 for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds, rowoff + 16u * q);
-                if constexpr (EFF) {
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[k] : 0u;
-                    tpc = lds_tools[(c >> 6) & 0x3FFu];
-                }
+                if constexpr (EFF) tpc = lds_tools[(c >> 6) & 0x3FFu];
             }
 #pragma unroll
             for (int i = 0; i < TC; ++i) {
                 uint4 mn[NQ];
-                uint32_t cn[4] = {0u, 0u, 0u, 0u}, tpn = 0u;
+                uint32_t tpn = 0u;
                 if constexpr (!PREF) {
                     const uint32_t c = ctl[i];
                     const uint32_t rowoff = ((c >> 16) << 4) + qoff;
 #pragma unroll
                     for (int q = 0; q < NQ; ++q) mc[q] = lds128(lds, rowoff + 16u * q);
-                    if constexpr (EFF) {
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) cc[k] = MULTI ? cq0[i * CNT_STRIDE + k] : 0u;
-                        tpc = lds_tools[(c >> 6) & 0x3FFu];
-                    }
+                    if constexpr (EFF) tpc = lds_tools[(c >> 6) & 0x3FFu];
                 }
                 if (PREF && i + 1 < TC) {
                     const uint32_t c = ctl[i + 1];
                     const uint32_t rowoff = ((c >> 16) << 4) + qoff;
 #pragma unroll
                     for (int q = 0; q < NQ; ++q) mn[q] = lds128(lds, rowoff + 16u * q);
-                    if constexpr (EFF) {
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) cn[k] = MULTI ? cq0[(i + 1) * CNT_STRIDE + k] : 0u;
-                        tpn = lds_tools[(c >> 6) & 0x3FFu];
-                    }
+                    if constexpr (EFF) tpn = lds_tools[(c >> 6) & 0x3FFu];
                 }
                 if ((uint32_t)i < nr) {
                     const uint32_t c = ctl[i];
@@ -1210,10 +1211,8 @@ struct ChainF {
                         const uint64_t bal = __ballot(dk);
                         uint32_t n1, rank_t;
                         if constexpr (MULTI) {
-                            n1 = (g[0] ? cc[0] : 0u) + (g[1] ? cc[1] : 0u) + (g[2] ? cc[2] : 0u) +
-                                 (g[3] ? cc[3] : 0u);
-                            rank_t = (f[0] ? cc[0] : 0u) + (f[1] ? cc[1] : 0u) + (f[2] ? cc[2] : 0u) +
-                                     lane_rank(bal);
+                            n1 = __builtin_amdgcn_readlane(n1v, i);
+                            rank_t = __builtin_amdgcn_readlane(prev, i) + lane_rank(bal);
                         } else {
                             const uint64_t bs = bal & L.seg;
                             n1 = (uint32_t)__popcll(bs);
@@ -1267,11 +1266,7 @@ struct ChainF {
                 if (PREF && i + 1 < TC) {
 #pragma unroll
                     for (int q = 0; q < NQ; ++q) mc[q] = mn[q];
-                    if constexpr (EFF) {
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) cc[k] = cn[k];
-                        tpc = tpn;
-                    }
+                    if constexpr (EFF) tpc = tpn;
                 }
             }
         };
