@@ -2072,13 +2072,32 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     h->cdf_off = h->full ? m0_words : tab_words;
     h->guide_off = h->cdf_off + pad4(h->ra.cdf_n);
     const uint32_t after_guide = h->full ? tab_words + pad4(R) : 0u;  // rows and tools
+    // The chain kernel's LDS after the image: the count exchange ([16][nwave +
+    // 4] words; the table chain uses the first [2][nwave + 4]), then (full
+    // image, WMAX >= 16: the two-role or the pipelined split) the control
+    // handed to the replaying lanes, 16 steps of a 4-byte addend and a 4-byte
+    // control word per lane, then (full image) the effect stage of
+    // sub-wavefront bins, 4 + 16 bytes per lane.
+    h->nwave = h->full ? 4u : 8u;
+    const bool ctl_area = h->full && h->wmax >= 16u;
+    const uint32_t na = h->nwave * 64u;
+    const size_t lds_after_image = 16u * (h->nwave + 4u) * 4u + (ctl_area ? 16u * na * 8u : 0u) +
+                                   (h->full ? na * 20u : 0u);
     uint32_t guide_bits = 0, guide_n = 0;
     if (h->ra.mode == RC_ROUTE_CDF) {
+        // Eight buckets per route, at most 2^12: with skewed routes the
+        // thresholds of the light routes crowd into few buckets, and every
+        // threshold in a bucket is a dependent LDS step of the chain's search
+        // (Zipf(1.1) over 64 routes: at most 1 per bucket, 2 with four
+        // buckets per route).  Fewer buckets when that keeps two workgroups
+        // on a CU that the smallest guide would allow.
         const uint32_t gmin = ceil_log2(R) < 1u ? 1u : ceil_log2(R);
-        guide_bits = gmin + 2u < 12u ? gmin + 2u : (gmin > 12u ? gmin : 12u);
-        while (guide_bits > gmin &&
-               ((size_t)h->guide_off + pad4((1u << guide_bits) + 1u) + after_guide) * 4u + 256u > lds_two_per_cu)
-            --guide_bits;
+        guide_bits = gmin + 3u < 12u ? gmin + 3u : (gmin > 12u ? gmin : 12u);
+        auto lds_at = [&](uint32_t gb) {
+            return ((size_t)h->guide_off + pad4((1u << gb) + 1u) + after_guide) * 4u + lds_after_image;
+        };
+        if (lds_at(gmin) <= lds_two_per_cu)
+            while (guide_bits > gmin && lds_at(guide_bits) > lds_two_per_cu) --guide_bits;
         guide_n = (1u << guide_bits) + 1u;
         h->ra.guide_shift = 32u - guide_bits;
     }
@@ -2088,20 +2107,11 @@ int rc_cohort_create(const rc_cohort_desc* desc, int hip_device, rc_cohort** out
     h->tools_off = h->rows_off + tab_words;
     h->img_words = h->full ? h->tools_off + pad4(R) : guide_end;
     const size_t lds_image = (size_t)h->img_words * 4u;
-    h->nwave = h->full ? 4u : 8u;
-    // image, then the count exchange ([16][nwave + 4] words; the table chain
-    // uses the first [2][nwave + 4]), then (full image, WMAX >= 16: the
-    // two-role or the pipelined split) the control handed to the replaying
-    // lanes, 16 steps of a 4-byte addend and a 4-byte control word per lane,
-    // then (full image) the effect stage of sub-wavefront bins, 4 + 16 bytes
-    // per lane.  chain_threads is the two-role (W >= 32) or one-lane
-    // workgroup; the pipelined split launches three lanes per session.
+    // chain_threads is the two-role (W >= 32) or one-lane workgroup; the
+    // pipelined split launches three lanes per session.
     const bool split = h->full && h->wmax >= 32u;
-    const bool ctl_area = h->full && h->wmax >= 16u;
-    const uint32_t na = h->nwave * 64u;
     h->chain_threads = (split ? 2u : 1u) * na;
-    h->chain_lds_bytes = lds_image + 16u * (h->nwave + 4u) * 4u + (ctl_area ? 16u * na * 8u : 0u) +
-                         (h->full ? na * 20u : 0u);
+    h->chain_lds_bytes = lds_image + lds_after_image;
 
     h->offsets.assign(desc->cohort_offsets, desc->cohort_offsets + h->C + 1u);
     build_plan(h->offsets.data(), h->C, h->nwave, h->plan);
