@@ -9,7 +9,12 @@ Two corners that the other parity tests do not reach:
 - the largest session count, N = 2^28 (1,048,578 cohorts, a ragged tail):
   sampled cohorts against the oracle, every effect slice checked to hold, at
   each slot, a session of the slot's cohort and all N sessions once, and the
-  host round trip equal to the resident chain over every output.
+  host round trip equal to the resident chain over every output;
+- the largest LDS footprint of a chain workgroup: the full mask image, which
+  every W <= 16 takes, with about a thousand CDF routes and their guide table
+  of 2^12 buckets -- about 146 KB of LDS per workgroup, one workgroup per CU,
+  the pipelined split -- against the oracle bit for bit, in both mechanisms
+  and over ragged cohort ranges.
 The first uses 77 GiB of device memory at W = 64, the second about 45 GiB.
 """
 import sys
@@ -181,3 +186,35 @@ def test_largest_session_count(orc):
             assert torch.equal(co2.t[k], co.t[k]), k
     finally:
         release(*(c for c in (co, co2) if c is not None))
+
+
+# (W, R, T, step0): full mask image at W <= 16 with ~1,000 CDF routes
+LDS_CASES = [(16, 1024, 9, 0), (13, 1000, 20, 0xFFFFFFF9), (9, 1024, 4, 77)]
+
+
+@pytest.mark.parametrize("case", range(len(LDS_CASES)))
+def test_largest_lds_footprint(orc, case):
+    W, R, T, step0 = LDS_CASES[case]
+    rng = np.random.Generator(np.random.PCG64(36_000 + case))
+    sizes = [int(x) for x in rng.choice([1, 17, 32, 63, 64, 65, 128, 200, 256], size=300)]
+    inp = wk.make_custom(n_words=W, n_routes=R, route_mode=wk.ROUTE_CDF, decide_thr=19661,
+                         cohort_sizes=sizes, n_steps=T, seed_key=36_100 + case)
+    C = inp.n_cohorts
+    say("largest LDS footprint: W=%d R=%d CDF C=%d N=%d T=%d step0=%d"
+        % (W, R, C, inp.n_sessions, T, step0))
+    want = orc.run_inputs(inp, n_steps=T, step0=step0)
+    cuts = sorted(set([0, C] + [int(x) for x in rng.integers(0, C + 1, size=3)]))
+    ranges = [(cuts[i], cuts[i + 1]) for i in range(len(cuts) - 1)]
+    rng.shuffle(ranges)
+    for label, mode, rr in (("resident", rc.RC_MODE_RESIDENT, [(0, C)]),
+                            ("resident ranges", rc.RC_MODE_RESIDENT, ranges),
+                            ("host round trip", rc.RC_MODE_HOST_ROUNDTRIP, [(0, C)])):
+        co = rc.Cohort.from_inputs(inp, max_steps=T)
+        try:
+            for cb, ce in rr:
+                co.run_chain(step0, T, mode, cb, ce)
+            got = co.download(T)
+        finally:
+            co.close()
+        for k in KEYS:
+            assert np.array_equal(got[k], want[k]), (case, label, k)
