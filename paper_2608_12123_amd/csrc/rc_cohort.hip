@@ -494,23 +494,23 @@ __device__ __forceinline__ uint32_t tool_of(const uint32_t* lds, const uint32_t*
 }
 
 // Table image, band 0 (words 4..15): masks table[r][j] * (j + 1).
-template <int J, bool EXACT, int WMAX>
+template <int J, int WMAX>
 __device__ __forceinline__ void band0(uint32_t (&S)[WMAX], const uint32_t (&tv)[16],
-                                      uint32_t (&M)[16], uint32_t sh, uint32_t oo, uint32_t W) {
+                                      uint32_t (&M)[16], uint32_t sh, uint32_t oo) {
     if constexpr (J < 16) {
         M[J] = mul_small<J + 1>(tv[J]);
         if constexpr (J < WMAX)
             S[J] = (rotr32(S[J], sh) ^ M[J]) + oo;  // words >= W: padding, see band()
-        band0<J + 1, EXACT, WMAX>(S, tv, M, sh, oo, W);
+        band0<J + 1, WMAX>(S, tv, M, sh, oo);
     }
 }
 
 // Table image, band B >= 1 (words 16 B .. 16 B + 15): the mask of w is the
 // mask of w - 16 plus table[r][w mod 16] << 4; it is formed only after word
 // w - 16 is done, so one band of masks is live at a time.
-template <int B, bool EXACT, int WMAX>
+template <int B, int WMAX>
 __device__ __forceinline__ void band(uint32_t (&S)[WMAX], const uint32_t (&tv)[16],
-                                     uint32_t (&M)[16], uint32_t sh, uint32_t oo, uint32_t W) {
+                                     uint32_t (&M)[16], uint32_t sh, uint32_t oo) {
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
         constexpr int base = 16 * B;
@@ -605,16 +605,16 @@ struct Chain {
             for (int w = 4; w < WMAX; ++w)
                 if (EXACT || (uint32_t)w < W) st.S[w] = (rotr32(st.S[w], sh) ^ mc[w]) + oo;
         } else {
-            band0<4, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
+            band0<4, WMAX>(st.S, mc, M, sh, oo);
             __builtin_amdgcn_sched_barrier(0);
             if constexpr (WMAX > 16) {
-                band<1, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
+                band<1, WMAX>(st.S, mc, M, sh, oo);
                 __builtin_amdgcn_sched_barrier(0);
             }
             if constexpr (WMAX > 32) {
-                band<2, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
+                band<2, WMAX>(st.S, mc, M, sh, oo);
                 __builtin_amdgcn_sched_barrier(0);
-                band<3, EXACT, WMAX>(st.S, mc, M, sh, oo, W);
+                band<3, WMAX>(st.S, mc, M, sh, oo);
             }
         }
 
@@ -1427,11 +1427,11 @@ struct ChainF {
 
 // One workgroup per bin: blocks [0, bins_a_n) take the sub-wavefront bins,
 // the rest the multi-wavefront bins.  The table-image chain and the two-role
-// full-image chain at W <= 32 run two 512-lane workgroups per CU, so they are
+// full-image chain at W = 32 run two 512-lane workgroups per CU, so they are
 // held to four wavefronts per SIMD (at most 128 VGPRs); the pipelined split
-// (W <= 32) runs two 768-lane workgroups per CU, six wavefronts per SIMD
-// (at most 80 VGPRs).  At W = 64 the two-lane full-image chain needs more registers and
-// runs one per CU.
+// (W = 16 or 32) runs two 768-lane workgroups per CU, six wavefronts per
+// SIMD (at most 80 VGPRs).  At W = 64 the two-role full-image chain needs
+// more registers and runs one workgroup per CU.
 template <int WMAX, bool EXACT, int NWAVE, bool FULL, int RK, bool FLOOR, bool PIPED>
 __global__ __launch_bounds__((FULL && (WMAX >= 32 || (PIPED && WMAX == 16)) ? (PIPED && WMAX <= 32 ? 3 : 2) : 1) *
                                  NWAVE * 64,
